@@ -1,0 +1,175 @@
+// GRPO group advantage with the gradient-filter compaction, and the live-row
+// compaction of ragged decoding.  Both are tiny (N <= a few thousand): one
+// workgroup of 1024 threads walks the input in chunks, and a ballot / mbcnt
+// prefix inside each wave plus an LDS scan across the 16 waves gives every
+// kept element its output slot, so kept indices come out in ascending order
+// with no atomics (deterministic).
+//
+// Group statistics (groups of G <= 64): samples are spread over "virtual
+// lanes", P2 = next power of two >= G lanes per group with the tail zero, so a
+// group sits in an aligned run of P2 lanes of one wave and an xor butterfly
+// (offsets 1, 2, 4, ...) forms the pairwise sum, adjacent pairs first.  Groups
+// with 64 < G <= 1024 use the same tree in LDS, one group at a time.
+// Built with -ffp-contract=off: see sampler_math.h.
+#include "common.h"
+#include "kernels.h"
+#include "sampler_math.h"
+
+namespace dash {
+
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+
+// Exclusive prefix of `flag` over the workgroup, in thread order; returns the
+// prefix and writes the total to *total.  `scan` is LDS of kWaves ints.
+DASH_DEV int block_excl_scan(bool flag, int* scan, int* total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t bal = __ballot(flag);
+    const int in_wave = __popcll(bal & ((1ull << lane) - 1ull));
+    __syncthreads();
+    if (lane == 0) scan[w] = __popcll(bal);
+    __syncthreads();
+    int before = 0, tot = 0;
+    for (int i = 0; i < kWaves; ++i) {
+        const int c = scan[i];
+        before += i < w ? c : 0;
+        tot += c;
+    }
+    *total = tot;
+    return before + in_wave;
+}
+
+DASH_DEV float adv_of(float d, float ss, int G, int mode, float eps) {
+    if (mode == 0) return d;
+    const int ddof = mode == 2 ? 1 : 0;
+    float sd = 0.f;
+    if (G - ddof > 0) sd = sqrt_rn(div_rn(ss, (float)(G - ddof)));
+    return div_rn(d, sd + eps);
+}
+
+__global__ void __launch_bounds__(kThreads) adv_filter_wave_k(const float* __restrict__ r, int n_groups, int G, int P2,
+                                                              int mode, float eps, float tau, float* __restrict__ adv,
+                                                              int32_t* __restrict__ kept, int32_t* __restrict__ count) {
+    __shared__ int scan[kWaves];
+    const int total_v = n_groups * P2;
+    int base = 0;
+    for (int c0 = 0; c0 < total_v; c0 += kThreads) {
+        const int v = c0 + threadIdx.x;
+        const int grp = v / P2, j = v % P2;
+        const bool valid = v < total_v && j < G;
+        const int n = grp * G + j;
+        const float x = valid ? r[n] : 0.f;
+        float s = x;
+        for (int o = 1; o < P2; o <<= 1) s = s + __shfl_xor(s, o, 64);
+        const float mu = div_rn(s, (float)G);
+        const float d = x - mu;
+        float q = valid ? d * d : 0.f;
+        if (mode != 0)
+            for (int o = 1; o < P2; o <<= 1) q = q + __shfl_xor(q, o, 64);
+        const float a = adv_of(d, q, G, mode, eps);
+        const bool keep = valid && fabsf(a) >= tau;
+        if (valid) adv[n] = a;
+        int tot;
+        const int at = block_excl_scan(keep, scan, &tot);
+        if (keep) kept[base + at] = n;
+        base += tot;
+    }
+    if (threadIdx.x == 0) *count = base;
+}
+
+__global__ void __launch_bounds__(kThreads) adv_filter_lds_k(const float* __restrict__ r, int n_groups, int G, int P2,
+                                                             int mode, float eps, float tau, float* __restrict__ adv,
+                                                             int32_t* __restrict__ kept, int32_t* __restrict__ count) {
+    __shared__ float buf[kThreads];
+    __shared__ int scan[kWaves];
+    const int j = threadIdx.x;
+    int base = 0;
+    for (int grp = 0; grp < n_groups; ++grp) {
+        const bool valid = j < G;
+        const int n = grp * G + j;
+        const float x = valid ? r[n] : 0.f;
+        if (j < P2) buf[j] = x;
+        __syncthreads();
+        for (int half = P2 >> 1; half >= 1; half >>= 1) {  // a[i] = a[2i] + a[2i+1]
+            float t = 0.f;
+            if (j < half) t = buf[2 * j] + buf[2 * j + 1];
+            __syncthreads();
+            if (j < half) buf[j] = t;
+            __syncthreads();
+        }
+        const float mu = div_rn(buf[0], (float)G);
+        const float d = x - mu;
+        __syncthreads();
+        if (j < P2) buf[j] = valid ? d * d : 0.f;
+        __syncthreads();
+        for (int half = P2 >> 1; half >= 1; half >>= 1) {
+            float t = 0.f;
+            if (j < half) t = buf[2 * j] + buf[2 * j + 1];
+            __syncthreads();
+            if (j < half) buf[j] = t;
+            __syncthreads();
+        }
+        const float a = adv_of(d, buf[0], G, mode, eps);
+        __syncthreads();
+        const bool keep = valid && fabsf(a) >= tau;
+        if (valid) adv[n] = a;
+        int tot;
+        const int at = block_excl_scan(keep, scan, &tot);
+        if (keep) kept[base + at] = n;
+        base += tot;
+    }
+    if (threadIdx.x == 0) *count = base;
+}
+
+__global__ void __launch_bounds__(kThreads)
+live_compact_k(const int32_t* __restrict__ tok, const int32_t* __restrict__ slot, const int32_t* __restrict__ pos,
+               const int32_t* __restrict__ step, const int32_t* __restrict__ uid, const int32_t* __restrict__ budget,
+               int eos_id, int n, int32_t* __restrict__ tok_o, int32_t* __restrict__ slot_o,
+               int32_t* __restrict__ pos_o, int32_t* __restrict__ step_o, int32_t* __restrict__ uid_o,
+               int32_t* __restrict__ count) {
+    __shared__ int scan[kWaves];
+    int base = 0;
+    for (int c0 = 0; c0 < n; c0 += kThreads) {
+        const int i = c0 + threadIdx.x;
+        bool live = false;
+        if (i < n) live = (step[i] + 1 < budget[uid[i]]) && !(eos_id >= 0 && tok[i] == eos_id);
+        int tot;
+        const int at = block_excl_scan(live, scan, &tot);
+        if (live) {
+            const int o = base + at;
+            tok_o[o] = tok[i];
+            slot_o[o] = slot[i];
+            pos_o[o] = pos[i] + 1;
+            step_o[o] = step[i] + 1;
+            uid_o[o] = uid[i];
+        }
+        base += tot;
+    }
+    if (threadIdx.x == 0) *count = base;
+}
+
+}  // namespace
+
+hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,
+                                         float* adv, int32_t* kept, int32_t* count, hipStream_t st) {
+    int P2 = 1;
+    while (P2 < group) P2 <<= 1;
+    if (P2 <= 64)
+        adv_filter_wave_k<<<1, kThreads, 0, st>>>(r, n_groups, group, P2, mode, eps, tau, adv, kept, count);
+    else
+        adv_filter_lds_k<<<1, kThreads, 0, st>>>(r, n_groups, group, P2, mode, eps, tau, adv, kept, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_live_compact(const int32_t* tok, const int32_t* slot, const int32_t* pos, const int32_t* step,
+                               const int32_t* uid, const int32_t* budget, int eos_id, int n, int32_t* tok_o,
+                               int32_t* slot_o, int32_t* pos_o, int32_t* step_o, int32_t* uid_o, int32_t* count,
+                               hipStream_t st) {
+    live_compact_k<<<1, kThreads, 0, st>>>(tok, slot, pos, step, uid, budget, eos_id, n, tok_o, slot_o, pos_o, step_o,
+                                           uid_o, count);
+    return hipGetLastError();
+}
+
+}  // namespace dash

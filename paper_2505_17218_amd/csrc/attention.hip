@@ -1,0 +1,319 @@
+// Attention over the paged KV cache.
+//
+// Decode (bf16): one wave per (row, kv head, context split).  All query heads
+// that share the kv head (GQA group, <= 16) ride in the N dimension of
+// v_mfma_f32_16x16x32_bf16:
+//   S^T[key, head] = K[key, :] . Q[head, :]      (A = K tile, B = Q^T)
+//   O^T[dim, head] += V^T[dim, key] . P^T[key, head]   (A = V^T tile, B = P^T)
+// The K page layout ([chunk of 32 dims][key][32]) and the transposed,
+// key-permuted V page layout make every A-operand load a 16-byte read per lane
+// and a contiguous 1 KB per wave, straight from HBM into VGPRs: nothing is
+// shared between waves, so there is no LDS round trip.  The S^T accumulator
+// gives each lane 4 consecutive keys of one head per 16-key half; those 8
+// probabilities are exactly the lane's P^T operand, so no shuffles are needed
+// between the two MFMAs.  Online softmax in fp32 (base 2), with per-lane partial
+// denominators reduced once at the end.  Long contexts are split across
+// workgroups and merged by a second kernel in a fixed order (deterministic).
+//
+// Generic (fp32 caches, and prefill of any dtype): one wave per (row, query
+// head), scores with lanes over keys and the value sum with lanes over dims.
+#include "common.h"
+#include "kernels.h"
+
+#include <algorithm>
+
+namespace dash {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int HD>
+__global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
+                                                         const int32_t* __restrict__ slot,
+                                                         const int32_t* __restrict__ page_table,
+                                                         const bf16_t* __restrict__ pool, KVGeom g, int layer,
+                                                         int n_heads, bf16_t* __restrict__ o, int max_splits,
+                                                         float* __restrict__ part, float scale_log2) {
+    constexpr int NC = HD / 32;  // 32-dim chunks (K-steps of the score MFMA)
+    constexpr int ND = HD / 16;  // 16-dim blocks of the output
+    const int lane = threadIdx.x;
+    const int n_kv = g.n_kv;
+    const int row = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv, split = blockIdx.y;
+    const int rep = n_heads / n_kv;
+    const int head = lane & 15, grp = lane >> 4;
+    const int ctx = pos[row] + 1;
+    const int sl = slot[row];
+    const int nblk = (ctx + 31) >> 5;
+    constexpr int per = kAttnSplitKeys / 32;  // key blocks per split
+    const int nsplit = min((nblk + per - 1) / per, max_splits);  // rows past max_ctx are not valid input
+    if (split >= nsplit) return;
+    const int b_begin = split * per;
+    const int b_end = min(nblk, b_begin + per);
+
+    // Q^T operand per 32-dim chunk: lane holds q[head][c*32 + grp*8 .. +8] (zero for padding heads).
+    bf16x8_t qf[NC];
+    {
+        const bf16_t* qrow = q + ((size_t)row * n_heads + kvh * rep + (head < rep ? head : 0)) * HD;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            uint4 v = head < rep ? *reinterpret_cast<const uint4*>(qrow + c * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+            qf[c] = __builtin_bit_cast(bf16x8_t, v);
+        }
+    }
+
+    f32x4_t acc[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    uint4 kr[2][NC], vr[ND];
+    auto load_block = [&](int b) {
+        const int key0 = b << 5;
+        int page = kv_page_of(g, page_table, sl, key0);
+        const bool ok = page >= 0;
+        page = ok ? page : 0;
+        const int kin = key0 % g.page_size;
+        const bf16_t* kb = pool + kv_block(g, layer, page, kvh, 0);
+        const bf16_t* vb = pool + kv_block(g, layer, page, kvh, 1);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                kr[h][c] = ok ? *reinterpret_cast<const uint4*>(kb + ((size_t)c * g.page_size + kin + h * 16 + head) * 32 +
+                                                                grp * 8)
+                              : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+            vr[d] = ok ? *reinterpret_cast<const uint4*>(vb + (size_t)(d * 16 + head) * g.page_size + kin + grp * 8)
+                       : make_uint4(0, 0, 0, 0);
+    };
+
+    for (int b = b_begin; b < b_end; ++b) {
+        load_block(b);
+        const int key0 = b << 5;
+        f32x4_t s[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            s[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[h][c]), qf[c], s[h],
+                                                               0, 0, 0);
+        }
+        // lane holds keys key0 + h*16 + grp*4 + r for head `head`
+        float t[8];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = key0 + h * 16 + grp * 4 + r;
+                const float v = key < ctx ? s[h][r] * scale_log2 : -INFINITY;
+                t[h * 4 + r] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = exp2f(m_run - m_new);
+        m_run = m_new;
+        float psum = 0.f;
+        uint32_t pk[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float p0 = exp2f(t[2 * i] - m_new), p1 = exp2f(t[2 * i + 1] - m_new);
+            psum += p0 + p1;
+            pk[i] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+        }
+        l_run = l_run * alpha + psum;
+        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+        // Keys past the context have p = 0; zero their V too, so stale pool contents
+        // (possibly non-finite) cannot leak in through 0 * inf.
+        if (key0 + 32 > ctx) {
+#pragma unroll
+            for (int d = 0; d < ND; ++d) {
+                uint32_t w[4] = {vr[d].x, vr[d].y, vr[d].z, vr[d].w};
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int kk = j < 4 ? grp * 4 + j : 16 + grp * 4 + (j - 4);
+                    if (key0 + kk >= ctx) w[j >> 1] &= (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+                }
+                vr[d] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < ND; ++d) {
+            acc[d] *= alpha;
+            acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vr[d]), pf, acc[d], 0, 0, 0);
+        }
+    }
+    l_run += __shfl_xor(l_run, 16, 64);
+    l_run += __shfl_xor(l_run, 32, 64);
+
+    // acc[d][r] = O^T[dim d*16 + grp*4 + r][head]
+    if (head >= rep) return;
+    const int qh = kvh * rep + head;
+    if (nsplit == 1) {  // the only split: normalise and store
+        const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+        bf16_t* orow = o + ((size_t)row * n_heads + qh) * HD;
+#pragma unroll
+        for (int d = 0; d < ND; ++d) {
+            const uint32_t lo = (uint32_t)f2bf(acc[d][0] * inv) | ((uint32_t)f2bf(acc[d][1] * inv) << 16);
+            const uint32_t hi = (uint32_t)f2bf(acc[d][2] * inv) | ((uint32_t)f2bf(acc[d][3] * inv) << 16);
+            *reinterpret_cast<uint2*>(orow + d * 16 + grp * 4) = make_uint2(lo, hi);
+        }
+    } else {
+        const size_t base = ((size_t)row * n_heads + qh) * max_splits + split;
+        float* op = part + base * HD;
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+            *reinterpret_cast<float4*>(op + d * 16 + grp * 4) = make_float4(acc[d][0], acc[d][1], acc[d][2], acc[d][3]);
+        if (grp == 0) {
+            float* ml = part + (size_t)(gridDim.x / n_kv) * n_heads * max_splits * HD + base * 2;
+            ml[0] = m_run;
+            ml[1] = l_run;
+        }
+    }
+}
+
+// Merge the context splits of rows that have more than one, in split order:
+// o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+template <typename T>
+__global__ void combine_k(const float* __restrict__ part, const int32_t* __restrict__ pos, int rows, int n_heads,
+                          int max_splits, int hd, T* __restrict__ o) {
+    const int rh = blockIdx.x;  // row * n_heads + head
+    const int row = rh / n_heads;
+    const int ns = min((pos[row] + kAttnSplitKeys) / kAttnSplitKeys, max_splits);  // ceil((pos + 1) / split keys)
+    if (ns <= 1) return;  // written directly by the attention kernel
+    const float* ml = part + (size_t)rows * n_heads * max_splits * hd + (size_t)rh * max_splits * 2;
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, ml[2 * s]);
+    float den = 0.f;
+    for (int s = 0; s < ns; ++s) den += exp2f(ml[2 * s] - M) * ml[2 * s + 1];
+    const float inv = den > 0.f ? 1.0f / den : 0.f;
+    for (int d = threadIdx.x; d < hd; d += blockDim.x) {
+        float num = 0.f;
+        for (int s = 0; s < ns; ++s) num += exp2f(ml[2 * s] - M) * part[((size_t)rh * max_splits + s) * hd + d];
+        st_elem(o + (size_t)rh * hd + d, num * inv);
+    }
+}
+
+// Generic paged attention: grid (rows, n_heads), one wave.  Row r attends to
+// positions 0..pos[r] of slot[r].
+template <typename T>
+__global__ void __launch_bounds__(64) attn_generic_k(const T* __restrict__ q, const int32_t* __restrict__ pos,
+                                                     const int32_t* __restrict__ slot,
+                                                     const int32_t* __restrict__ page_table,
+                                                     const T* __restrict__ pool, KVGeom g, int layer, int n_heads,
+                                                     T* __restrict__ o, float scale) {
+    __shared__ float qs[128];
+    __shared__ float ps[64];
+    __shared__ int pg[64];
+    const int row = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int hd = g.head_dim, rep = n_heads / g.n_kv, kvh = h / rep;
+    const int ctx = pos[row] + 1, sl = slot[row];
+    const T* qrow = q + ((size_t)row * n_heads + h) * hd;
+    for (int d = lane; d < hd; d += 64) qs[d] = ld_elem(qrow + d);
+    __syncthreads();
+    float m_run = -INFINITY, l_run = 0.f, acc0 = 0.f, acc1 = 0.f;
+    for (int base = 0; base < ctx; base += 64) {
+        const int key = base + lane;
+        float s = -INFINITY;
+        int page = -1;
+        if (key < ctx) {
+            page = kv_page_of(g, page_table, sl, key);
+            if (page >= 0) {
+                const T* kb = pool + kv_block(g, layer, page, kvh, 0);
+                const int kin = key % g.page_size;
+                float dot = 0.f;
+                for (int d = 0; d < hd; ++d) dot += qs[d] * ld_elem(kb + k_index<T>(g, kin, d));
+                s = dot * scale;
+            }
+        }
+        const float cmax = wave_max(s);
+        const float m_new = fmaxf(m_run, cmax);
+        const float alpha = m_new == -INFINITY ? 1.f : __expf(m_run - m_new);
+        const float p = s == -INFINITY ? 0.f : __expf(s - m_new);
+        l_run = l_run * alpha + wave_sum(p);
+        acc0 *= alpha;
+        acc1 *= alpha;
+        m_run = m_new;
+        ps[lane] = p;
+        pg[lane] = page;
+        __syncthreads();
+        const int n = min(64, ctx - base);
+        for (int j = 0; j < n; ++j) {
+            const float pj = ps[j];
+            const int pgj = pg[j];
+            if (pj == 0.f || pgj < 0) continue;
+            const T* vb = pool + kv_block(g, layer, pgj, kvh, 1);
+            const int kin = (base + j) % g.page_size;
+            if (lane < hd) acc0 += pj * ld_elem(vb + v_index<T>(g, kin, lane));
+            if (lane + 64 < hd) acc1 += pj * ld_elem(vb + v_index<T>(g, kin, lane + 64));
+        }
+        __syncthreads();
+    }
+    const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+    T* orow = o + ((size_t)row * n_heads + h) * hd;
+    if (lane < hd) st_elem(orow + lane, acc0 * inv);
+    if (lane + 64 < hd) st_elem(orow + lane + 64, acc1 * inv);
+}
+
+}  // namespace
+
+size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx) {
+    const int ms = (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys;
+    if (ms <= 1) return 0;
+    return (size_t)rows * n_heads * ms * (head_dim + 2);
+}
+
+hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
+                                   const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                   int n_heads, void* o, int rows, int max_ctx, float* ws_part, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    const float scale = 1.0f / sqrtf((float)g.head_dim);
+    if (dtype == 1) {
+        const int ms = std::max(1, (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys);
+        dim3 grid(rows * g.n_kv, ms);
+        const float sl2 = scale * kLog2e;
+        if (g.head_dim == 128)
+            decode_attn_bf16_k<128><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
+                                                          g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2);
+        else if (g.head_dim == 64)
+            decode_attn_bf16_k<64><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
+                                                         g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
+    dim3 grid(rows, n_heads);
+    attn_generic_k<float><<<grid, 64, 0, st>>>((const float*)q, pos, slot, page_table, (const float*)pool, g, layer,
+                                               n_heads, (float*)o, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
+                                    int max_ctx, const float* ws_part, void* o, hipStream_t st) {
+    const int ms = (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys;
+    if (dtype != 1 || ms <= 1 || rows <= 0) return hipSuccess;
+    combine_k<bf16_t><<<rows * n_heads, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, head_dim, (bf16_t*)o);
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
+                                    const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                    int n_heads, void* o, int rows, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    const float scale = 1.0f / sqrtf((float)g.head_dim);
+    dim3 grid(rows, n_heads);
+    if (dtype == 1)
+        attn_generic_k<bf16_t><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool, g,
+                                                    layer, n_heads, (bf16_t*)o, scale);
+    else
+        attn_generic_k<float><<<grid, 64, 0, st>>>((const float*)q, pos, slot, page_table, (const float*)pool, g,
+                                                   layer, n_heads, (float*)o, scale);
+    return hipGetLastError();
+}
+
+}  // namespace dash

@@ -1,0 +1,82 @@
+// Host-side launchers of the HIP kernels.  All launch on `st` and return the
+// hipError_t of the launch.  Shapes are validated by the caller (runtime.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dash {
+
+struct KVGeom;
+
+// ---- elementwise (elementwise.hip) ----
+// x[r] = E[tok[r]] (fp32); y[r] = RMSNorm(x[r]) * w in the model dtype.
+// Token ids are clamped to [0, vocab) so a bad id can never index outside E.
+hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, const void* w, float* x, void* y,
+                                int rows, int d, int vocab, float eps, hipStream_t st);
+// For output row i, r = row_map ? row_map[i] : i: v = x[r] + sum_s delta[s*split_stride + r*d];
+// if write_x, x[r] = v; y[i] = RMSNorm(v) * w.
+hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nsplit, size_t split_stride,
+                              const void* w, void* y, const int32_t* row_map, int rows, int d, float eps,
+                              int write_x, hipStream_t st);
+// cos/sin table [rows][head_dim/2][2] of pos[r] * theta^(-2i/head_dim), evaluated in float64.
+hipError_t launch_rope_table(const int32_t* pos, float* cs, int rows, int head_dim, float theta, hipStream_t st);
+// qkv (sum of nsplit fp32 partials) + bias; RoPE on q and k; q -> q_out (model dtype,
+// [rows][Hq][hd]); k, v -> KV pages of (slot[r], pos[r]) at `layer`.
+hipError_t launch_qkv_rope_append(int dtype, const float* qkv, int nsplit, size_t split_stride, const void* bias,
+                                  const float* cs, const int32_t* pos, const int32_t* slot,
+                                  const int32_t* page_table, void* pool, const KVGeom& g, int layer,
+                                  void* q_out, int rows, int n_heads, uint32_t* status, hipStream_t st);
+// Copy every layer of `src_page` to `dst_pages[i]` (i < n).
+hipError_t launch_copy_pages(int dtype, void* pool, const KVGeom& g, const int32_t* pairs, int n,
+                             hipStream_t st);
+// Rollout row state helpers.
+hipError_t launch_rows_init(int32_t* slot, int32_t* uid, int32_t* pos, int32_t* step, int n, int pos0, int step0,
+                            hipStream_t st);
+hipError_t launch_rows_advance(int32_t* pos, int32_t* step, int n, hipStream_t st);
+hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st);
+hipError_t launch_iota_div(int32_t* p, int n, int div, hipStream_t st);  // p[i] = i / div
+
+// ---- GEMM (gemm.hip) ----
+enum { EPI_STORE_F32 = 0, EPI_SWIGLU = 1 };
+// C = A[M,K] . W[N,K]^T with fp32 accumulation.
+//   EPI_STORE_F32: C fp32 (row stride ldc) ; split-K into nsplit partials at C + s*split_stride.
+//   EPI_SWIGLU:    W rows [0, N/2) are gate, [N/2, N) up; writes h[M, N/2] (model dtype, row stride ldc)
+//                  = silu(gate) * up.  nsplit must be 1.
+hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C, int M, int N, int K, int ldc,
+                       int nsplit, size_t split_stride, hipStream_t st);
+// Split-K count for a weight of N x K (independent of M: results are batch-invariant).
+int gemm_pick_splits(int dtype, int epi, int N, int K);
+
+// ---- attention (attention.hip) ----
+// Decode attention over the paged cache for rows with 1 query each.  bf16: MFMA
+// kernel; a row's context is cut into splits of kAttnSplitKeys keys (depending on
+// its own length only, so results are batch-invariant) merged by a second kernel;
+// partials live in ws_part (attention_partial_floats).  fp32: generic kernel.
+// q [rows][Hq][hd]; o [rows][Hq*hd].
+constexpr int kAttnSplitKeys = 512;
+hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
+                                   const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                   int n_heads, void* o, int rows, int max_ctx, float* ws_part, hipStream_t st);
+size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx);
+// Second pass of decode attention: merge the splits of rows longer than one split (bf16 only).
+hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
+                                    int max_ctx, const float* ws_part, void* o, hipStream_t st);
+// Causal attention of prefill rows (generic kernel; row r attends to 0..pos[r] of slot[r]).
+hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
+                                    const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                    int n_heads, void* o, int rows, hipStream_t st);
+
+// ---- sampling / advantage (sampler.hip, advantage.hip) ----
+hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
+                         const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
+                         int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,
+                         hipStream_t st);
+hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,
+                                         float* adv, int32_t* kept, int32_t* count, hipStream_t st);
+hipError_t launch_live_compact(const int32_t* tok, const int32_t* slot, const int32_t* pos, const int32_t* step,
+                               const int32_t* uid, const int32_t* budget, int eos_id, int n, int32_t* tok_o,
+                               int32_t* slot_o, int32_t* pos_o, int32_t* step_o, int32_t* uid_o, int32_t* count,
+                               hipStream_t st);
+
+}  // namespace dash

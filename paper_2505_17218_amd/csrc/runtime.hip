@@ -1,0 +1,942 @@
+// Host runtime behind include/dash.h: argument checks, model and paged-KV
+// handles (page free list, reference counts, group fork with copy of a partial
+// last page), workspace planning, the prefill / decode-step sequencing of the
+// kernels, and the native rollout driver (reservation one page ahead, ragged
+// retirement, optional HIP-graph replay of the fixed-batch decode step).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <tuple>
+#include <string>
+#include <vector>
+
+#include "../../include/dash.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace dash;
+
+// ---------------------------------------------------------------- errors ----
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+#define DASH_HIP(call)                                                                              \
+    do {                                                                                            \
+        hipError_t e_ = (call);                                                                     \
+        if (e_ != hipSuccess) return fail(DASH_EDEVICE, "%s: %s", #call, hipGetErrorString(e_));   \
+    } while (0)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ------------------------------------------------------------- profiler ----
+// Event pairs around launches, by kernel class; a ring of pairs is harvested
+// lazily (a pair is read back only when its slot is reused or on read-out).
+
+struct Profiler {
+    struct Pair {
+        hipEvent_t a = nullptr, b = nullptr;
+        int cls = 0;
+        bool live = false;
+    };
+    uint32_t mask = 0;
+    bool capturing = false;
+    std::vector<Pair> ring;
+    size_t next = 0;
+    double ms[DASH_K_COUNT] = {};
+    int64_t n[DASH_K_COUNT] = {};
+};
+Profiler g_prof;
+
+void prof_harvest(Profiler::Pair& p) {
+    if (!p.live) return;
+    float ms = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+        g_prof.ms[p.cls] += ms;
+        g_prof.n[p.cls] += 1;
+    }
+    p.live = false;
+}
+
+// Times the launches made during its lifetime if class `cls` is enabled (cls < 0: never).
+struct ProfScope {
+    int slot = -1;
+    hipStream_t st;
+    ProfScope(int cls, hipStream_t s) : st(s) {
+        if (cls < 0 || !(g_prof.mask & (1u << cls)) || g_prof.capturing || g_prof.ring.empty()) return;
+        Profiler::Pair& p = g_prof.ring[g_prof.next];
+        prof_harvest(p);
+        if (hipEventRecord(p.a, st) != hipSuccess) return;
+        p.cls = cls;
+        slot = (int)g_prof.next;
+        g_prof.next = (g_prof.next + 1) % g_prof.ring.size();
+    }
+    ~ProfScope() {
+        if (slot < 0) return;
+        Profiler::Pair& p = g_prof.ring[slot];
+        p.live = hipEventRecord(p.b, st) == hipSuccess;
+    }
+};
+
+}  // namespace
+
+// ----------------------------------------------------------------- model ----
+
+struct dash_model {
+    dash_model_desc d;
+    std::vector<const void*> w;
+    size_t esz;
+    int qkv_rows() const { return (d.n_heads + 2 * d.n_kv_heads) * d.head_dim; }
+    const void* embed() const { return w[0]; }
+    const void* final_norm() const { return w[1]; }
+    const void* lw(int l, int i) const { return w[3 + 7 * l + i]; }
+};
+
+// -------------------------------------------------------------------- kv ----
+
+struct dash_kv {
+    const dash_model* m;
+    void* pool;
+    int32_t* d_table;
+    uint32_t* d_status;
+    KVGeom g;
+    int max_ctx;
+    std::vector<int32_t> table;   // [max_seqs][max_pages], -1 = none
+    std::vector<int32_t> len;     // per slot
+    std::vector<int32_t> npages;  // pages mapped per slot
+    std::vector<int32_t> refc;    // per page
+    std::vector<int32_t> free_list;
+    // pinned staging ring for uploads (two halves, each guarded by an event)
+    char* stage = nullptr;
+    size_t stage_half = 0;
+    int stage_cur = 0;
+    size_t stage_off = 0;
+    hipEvent_t stage_ev[2] = {nullptr, nullptr};
+    bool stage_ev_live[2] = {false, false};
+};
+
+namespace {
+
+size_t table_entries(int max_seqs, int max_ctx, int ps) {
+    return (size_t)max_seqs * (size_t)((max_ctx + ps - 1) / ps);
+}
+
+// Copy host bytes to device memory on `st` through the pinned ring.
+int kv_upload(dash_kv* kv, void* dst, const void* src, size_t bytes, hipStream_t st) {
+    if (bytes == 0) return DASH_OK;
+    size_t done = 0;
+    while (done < bytes) {
+        if (kv->stage_off >= kv->stage_half) {  // switch halves
+            DASH_HIP(hipEventRecord(kv->stage_ev[kv->stage_cur], st));
+            kv->stage_ev_live[kv->stage_cur] = true;
+            kv->stage_cur ^= 1;
+            kv->stage_off = 0;
+            if (kv->stage_ev_live[kv->stage_cur]) DASH_HIP(hipEventSynchronize(kv->stage_ev[kv->stage_cur]));
+        }
+        const size_t n = std::min(bytes - done, kv->stage_half - kv->stage_off);
+        char* p = kv->stage + kv->stage_cur * kv->stage_half + kv->stage_off;
+        memcpy(p, (const char*)src + done, n);
+        DASH_HIP(hipMemcpyAsync((char*)dst + done, p, n, hipMemcpyHostToDevice, st));
+        kv->stage_off = align_up(kv->stage_off + n, 256);
+        done += n;
+    }
+    return DASH_OK;
+}
+
+// Upload page-table rows [s0, s1] of the host mirror.
+int kv_push_rows(dash_kv* kv, int s0, int s1, hipStream_t st) {
+    if (s1 < s0) return DASH_OK;
+    const size_t mp = kv->g.max_pages;
+    return kv_upload(kv, kv->d_table + s0 * mp, kv->table.data() + s0 * mp, (size_t)(s1 - s0 + 1) * mp * 4, st);
+}
+
+int kv_alloc_page(dash_kv* kv) {
+    const int p = kv->free_list.back();
+    kv->free_list.pop_back();
+    kv->refc[p] = 1;
+    return p;
+}
+
+void kv_unref(dash_kv* kv, int p) {
+    if (--kv->refc[p] == 0) kv->free_list.push_back(p);
+}
+
+// Map pages so that positions [0, new_len) of `slot` are backed (host mirror only;
+// the caller uploads the rows).  The caller has checked that enough pages are free.
+void kv_grow(dash_kv* kv, int slot, int new_len) {
+    const int want = (new_len + kv->g.page_size - 1) / kv->g.page_size;
+    while (kv->npages[slot] < want) {
+        kv->table[(size_t)slot * kv->g.max_pages + kv->npages[slot]] = kv_alloc_page(kv);
+        kv->npages[slot]++;
+    }
+    kv->len[slot] = std::max(kv->len[slot], new_len);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------- workspace ----
+
+namespace {
+
+struct Ws {
+    float* x;
+    void* y;
+    float* qkv;
+    void* q;
+    void* o;
+    float* delta;
+    void* h;
+    float* cs;
+    float* attn_part;
+    int32_t* pos;    // prefill rows
+    int32_t* slot;   // prefill rows
+    int32_t* pslot;  // prefill prompt -> slot
+    int32_t* gather; // prefill last rows
+    int32_t* pairs;  // fork copies
+    size_t bytes;
+};
+
+// max_ctx bounds the decode attention's context splits (0: no decode use).
+Ws plan_ws(const dash_model* m, int max_rows, char* base, int max_ctx) {
+    const auto& d = m->d;
+    const size_t e = m->esz;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char* p = base ? base + off : nullptr;
+        off = align_up(off + bytes, 256);
+        return p;
+    };
+    Ws w{};
+    const size_t R = (size_t)max_rows;
+    const int qr = m->qkv_rows();
+    w.x = (float*)take(R * d.d_model * 4);
+    w.y = take(R * d.d_model * e);
+    w.qkv = (float*)take((size_t)gemm_pick_splits(d.dtype, EPI_STORE_F32, qr, d.d_model) * R * qr * 4);
+    w.q = take(R * d.n_heads * d.head_dim * e);
+    w.o = take(R * d.n_heads * d.head_dim * e);
+    const int so = gemm_pick_splits(d.dtype, EPI_STORE_F32, d.d_model, d.n_heads * d.head_dim);
+    const int sd = gemm_pick_splits(d.dtype, EPI_STORE_F32, d.d_model, d.d_ff);
+    w.delta = (float*)take((size_t)std::max(so, sd) * R * d.d_model * 4);
+    w.h = take(R * d.d_ff * e);
+    w.cs = (float*)take(R * d.head_dim * 4);
+    w.attn_part = (float*)take(attention_partial_floats(max_rows, d.n_heads, d.head_dim, max_ctx) * 4);
+    w.pos = (int32_t*)take(R * 4);
+    w.slot = (int32_t*)take(R * 4);
+    w.pslot = (int32_t*)take(R * 4);
+    w.gather = (int32_t*)take(R * 4);
+    w.pairs = (int32_t*)take(R * 8);
+    w.bytes = off;
+    return w;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------- ABI ----
+
+extern "C" {
+
+int dash_abi_version(void) { return DASH_ABI_VERSION; }
+
+const char* dash_status_str(int s) {
+    switch (s) {
+        case DASH_OK: return "ok";
+        case DASH_EINVAL: return "invalid argument";
+        case DASH_ENOMEM: return "out of host memory";
+        case DASH_ECAPACITY: return "capacity exceeded (pool, page table or workspace)";
+        case DASH_EDEVICE: return "HIP runtime error";
+        case DASH_ENOTSUP: return "shape not supported by the kernels";
+        default: return "unknown status";
+    }
+}
+
+const char* dash_last_error(void) { return g_last_error.c_str(); }
+
+int32_t dash_weight_count(const dash_model_desc* d) { return d && d->n_layers > 0 ? 3 + 7 * d->n_layers : -1; }
+
+int dash_model_create(const dash_model_desc* d, const void* const* w, int32_t n_w, dash_model** out) {
+    if (!d || !w || !out) return fail(DASH_EINVAL, "dash_model_create: NULL argument");
+    *out = nullptr;
+    if (d->n_layers < 1 || d->d_model < 1 || d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 2 ||
+        d->d_ff < 1 || d->vocab < 1)
+        return fail(DASH_EINVAL, "dash_model_create: non-positive dimension");
+    if (d->n_heads % d->n_kv_heads) return fail(DASH_EINVAL, "n_heads %% n_kv_heads != 0");
+    if (d->head_dim % 2) return fail(DASH_EINVAL, "head_dim must be even (RoPE pairs)");
+    if (d->dtype != DASH_F32 && d->dtype != DASH_BF16) return fail(DASH_EINVAL, "dtype must be DASH_F32 or DASH_BF16");
+    if (!(d->rope_theta > 0.f) || !(d->rms_eps >= 0.f)) return fail(DASH_EINVAL, "bad rope_theta or rms_eps");
+    if (n_w != dash_weight_count(d)) return fail(DASH_EINVAL, "expected %d weight pointers, got %d", dash_weight_count(d), n_w);
+    if (d->dtype == DASH_BF16) {
+        if (d->head_dim != 64 && d->head_dim != 128) return fail(DASH_ENOTSUP, "bf16 head_dim must be 64 or 128");
+        if (d->d_model % 64 || d->d_ff % 64) return fail(DASH_ENOTSUP, "bf16 d_model and d_ff must be multiples of 64");
+        if (d->n_heads / d->n_kv_heads > 16) return fail(DASH_ENOTSUP, "GQA group larger than 16");
+    } else {
+        if (d->head_dim > 128) return fail(DASH_ENOTSUP, "fp32 head_dim must be <= 128");
+        if (d->d_model % 4 || d->d_ff % 4) return fail(DASH_ENOTSUP, "fp32 d_model and d_ff must be multiples of 4");
+    }
+    for (int i = 0; i < n_w; ++i) {
+        if (i == 2) {
+            if (w[i]) return fail(DASH_ENOTSUP, "untied lm_head is not supported (pass NULL)");
+            continue;
+        }
+        if (!w[i]) return fail(DASH_EINVAL, "weight %d is NULL", i);
+        if ((uintptr_t)w[i] & 15) return fail(DASH_EINVAL, "weight %d is not 16-byte aligned", i);
+    }
+    dash_model* m = new (std::nothrow) dash_model;
+    if (!m) return fail(DASH_ENOMEM, "out of host memory");
+    m->d = *d;
+    m->w.assign(w, w + n_w);
+    m->esz = d->dtype == DASH_BF16 ? 2 : 4;
+    *out = m;
+    return DASH_OK;
+}
+
+void dash_model_destroy(dash_model* m) { delete m; }
+
+size_t dash_kv_page_bytes(const dash_model* m, int32_t ps) {
+    if (!m || ps < 1) return 0;
+    return (size_t)m->d.n_layers * m->d.n_kv_heads * 2 * (size_t)ps * m->d.head_dim * m->esz;
+}
+
+size_t dash_kv_table_bytes(int32_t max_seqs, int32_t max_ctx, int32_t ps) {
+    if (max_seqs < 1 || max_ctx < 1 || ps < 1) return 0;
+    return align_up(table_entries(max_seqs, max_ctx, ps) * 4, 256) + 256;
+}
+
+int dash_kv_create(const dash_model* m, void* pool, size_t pool_bytes, int32_t ps, int32_t max_seqs, int32_t max_ctx,
+                   void* d_table, void* stream, dash_kv** out) {
+    if (!m || !pool || !d_table || !out) return fail(DASH_EINVAL, "dash_kv_create: NULL argument");
+    *out = nullptr;
+    if (ps < 1 || ps > 1024 || max_seqs < 1 || max_ctx < 1) return fail(DASH_EINVAL, "dash_kv_create: bad sizes");
+    if (m->d.dtype == DASH_BF16 && ps % 32) return fail(DASH_ENOTSUP, "bf16 page_size must be a multiple of 32");
+    if ((uintptr_t)pool & 255) return fail(DASH_EINVAL, "pool must be 256-byte aligned");
+    const size_t pb = dash_kv_page_bytes(m, ps);
+    const size_t pages = pool_bytes / pb;
+    if (pages < 1) return fail(DASH_ECAPACITY, "pool holds no page (%zu bytes per page)", pb);
+    if (pages > 0x7FFFFFFF) return fail(DASH_EINVAL, "too many pages");
+    dash_kv* kv = new (std::nothrow) dash_kv;
+    if (!kv) return fail(DASH_ENOMEM, "out of host memory");
+    kv->m = m;
+    kv->pool = pool;
+    kv->max_ctx = max_ctx;
+    const int max_pages = (max_ctx + ps - 1) / ps;
+    kv->g = KVGeom{m->d.n_layers, (int)pages, m->d.n_kv_heads, m->d.head_dim, ps, max_pages, max_seqs};
+    const size_t ent = table_entries(max_seqs, max_ctx, ps);
+    kv->d_table = (int32_t*)d_table;
+    kv->d_status = (uint32_t*)((char*)d_table + align_up(ent * 4, 256));
+    kv->table.assign(ent, -1);
+    kv->len.assign(max_seqs, 0);
+    kv->npages.assign(max_seqs, 0);
+    kv->refc.assign(pages, 0);
+    kv->free_list.resize(pages);
+    for (size_t i = 0; i < pages; ++i) kv->free_list[i] = (int32_t)(pages - 1 - i);  // pop_back gives 0, 1, 2...
+    kv->stage_half = std::max<size_t>(align_up(ent * 4, 256), 1 << 16);
+    hipError_t e = hipHostMalloc((void**)&kv->stage, 2 * kv->stage_half, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        delete kv;
+        return fail(DASH_EDEVICE, "hipHostMalloc of the staging ring: %s", hipGetErrorString(e));
+    }
+    for (int i = 0; i < 2; ++i) {
+        e = hipEventCreateWithFlags(&kv->stage_ev[i], hipEventDisableTiming);
+        if (e != hipSuccess) {
+            dash_kv_destroy(kv);
+            return fail(DASH_EDEVICE, "hipEventCreate: %s", hipGetErrorString(e));
+        }
+    }
+    hipStream_t st = (hipStream_t)stream;
+    e = launch_fill_i32(kv->d_table, -1, ent, st);
+    if (e == hipSuccess) e = launch_fill_i32((int32_t*)kv->d_status, 0, 1, st);
+    if (e != hipSuccess) {
+        dash_kv_destroy(kv);
+        return fail(DASH_EDEVICE, "clearing the page table: %s", hipGetErrorString(e));
+    }
+    *out = kv;
+    return DASH_OK;
+}
+
+void dash_kv_destroy(dash_kv* kv) {
+    if (!kv) return;
+    for (int i = 0; i < 2; ++i) {
+        if (kv->stage_ev[i]) {
+            if (kv->stage_ev_live[i]) (void)hipEventSynchronize(kv->stage_ev[i]);
+            (void)hipEventDestroy(kv->stage_ev[i]);
+        }
+    }
+    if (kv->stage) {
+        (void)hipDeviceSynchronize();  // uploads still in flight read the ring
+        (void)hipHostFree(kv->stage);
+    }
+    delete kv;
+}
+
+int dash_kv_free_pages(const dash_kv* kv, int32_t* out) {
+    if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
+    *out = (int32_t)kv->free_list.size();
+    return DASH_OK;
+}
+
+int dash_kv_slot_len(const dash_kv* kv, int32_t slot, int32_t* out) {
+    if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
+    if (slot < 0 || slot >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", slot);
+    *out = kv->len[slot];
+    return DASH_OK;
+}
+
+int dash_kv_reserve(dash_kv* kv, const int32_t* h_slots, int32_t n, int32_t new_len, void* stream) {
+    if (!kv || (n > 0 && !h_slots)) return fail(DASH_EINVAL, "NULL argument");
+    if (n < 0 || new_len < 0) return fail(DASH_EINVAL, "negative count or length");
+    if (new_len > kv->max_ctx) return fail(DASH_ECAPACITY, "new_len %d exceeds max_ctx %d", new_len, kv->max_ctx);
+    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    size_t need = 0;
+    for (int i = 0; i < n; ++i) {
+        const int s = h_slots[i];
+        if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
+        const int want = (new_len + ps - 1) / ps;
+        if (want > kv->npages[s]) need += want - kv->npages[s];
+    }
+    // duplicates in h_slots would double count: harmless (over-estimate)
+    if (need > kv->free_list.size())
+        return fail(DASH_ECAPACITY, "pool exhausted: need %zu pages, %zu free", need, kv->free_list.size());
+    (void)mp;
+    int lo = kv->g.max_seqs, hi = -1;
+    for (int i = 0; i < n; ++i) {
+        const int s = h_slots[i];
+        const int before = kv->npages[s];
+        kv_grow(kv, s, new_len);
+        if (kv->npages[s] != before) {
+            lo = std::min(lo, s);
+            hi = std::max(hi, s);
+        }
+    }
+    return kv_push_rows(kv, lo, hi, (hipStream_t)stream);
+}
+
+int dash_kv_release(dash_kv* kv, const int32_t* h_slots, int32_t n) {
+    if (!kv || (n > 0 && !h_slots)) return fail(DASH_EINVAL, "NULL argument");
+    const int mp = kv->g.max_pages;
+    for (int i = 0; i < n; ++i) {
+        const int s = h_slots[i];
+        if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
+        for (int j = 0; j < kv->npages[s]; ++j) {
+            kv_unref(kv, kv->table[(size_t)s * mp + j]);
+            kv->table[(size_t)s * mp + j] = -1;
+        }
+        kv->npages[s] = 0;
+        kv->len[s] = 0;
+    }
+    // The device rows keep stale page ids until the slot is reused (the next
+    // reserve / prefill of the slot uploads its row); nothing reads a released slot.
+    return DASH_OK;
+}
+
+int dash_kv_device_status(dash_kv* kv, uint32_t* out, void* stream) {
+    if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
+    hipStream_t st = (hipStream_t)stream;
+    DASH_HIP(hipMemcpyAsync(out, kv->d_status, 4, hipMemcpyDeviceToHost, st));
+    DASH_HIP(hipStreamSynchronize(st));
+    DASH_HIP(launch_fill_i32((int32_t*)kv->d_status, 0, 1, st));
+    return DASH_OK;
+}
+
+size_t dash_workspace_bytes(const dash_model* m, int32_t max_rows, int32_t max_ctx) {
+    if (!m || max_rows < 1) return 0;
+    if (max_ctx < 0) return 0;
+    return plan_ws(m, max_rows, nullptr, max_ctx).bytes;
+}
+
+int dash_profile_enable(uint32_t class_mask) {
+    if (class_mask && g_prof.ring.empty()) {
+        g_prof.ring.resize(8192);
+        for (auto& p : g_prof.ring) {
+            if (hipEventCreate(&p.a) != hipSuccess || hipEventCreate(&p.b) != hipSuccess) {
+                g_prof.ring.clear();
+                return fail(DASH_EDEVICE, "hipEventCreate failed");
+            }
+        }
+    }
+    g_prof.mask = class_mask & ((1u << DASH_K_COUNT) - 1u);
+    return DASH_OK;
+}
+
+int dash_profile_read(double* ms_out, int64_t* launches_out, int32_t reset) {
+    for (auto& p : g_prof.ring) prof_harvest(p);
+    for (int i = 0; i < DASH_K_COUNT; ++i) {
+        if (ms_out) ms_out[i] = g_prof.ms[i];
+        if (launches_out) launches_out[i] = g_prof.n[i];
+        if (reset) {
+            g_prof.ms[i] = 0;
+            g_prof.n[i] = 0;
+        }
+    }
+    return DASH_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------- forward passes ----
+
+namespace {
+
+int ws_rows_for(const dash_model* m, size_t ws_bytes, int want) {
+    // largest row count <= want whose plan fits (plans grow monotonically in rows)
+    if (plan_ws(m, want, nullptr, 0).bytes <= ws_bytes) return want;
+    int lo = 0, hi = want;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (plan_ws(m, mid, nullptr, 0).bytes <= ws_bytes) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+// Transformer body over `rows` rows whose x/y are already set (x fp32, y = RMSNorm(x) * attn_norm[0]).
+// prefill: attention via the generic causal kernel over the rows' own slots; decode: MFMA paged kernel.
+// Leaves x updated by the last layer's down projection in (x, delta split partials) and
+// returns the split count of the last delta via *last_split.
+int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t* pos, const int32_t* slot,
+               bool prefill, hipStream_t st, int* last_split) {
+    const auto& d = m->d;
+    const int dt = d.dtype;
+    const int qr = m->qkv_rows();
+    const int hq = d.n_heads * d.head_dim;
+    const int sq = gemm_pick_splits(dt, EPI_STORE_F32, qr, d.d_model);
+    const int so = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, hq);
+    const int sd = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, d.d_ff);
+    auto cls = [&](int c) { return prefill ? -1 : c; };  // prefill is timed as one class by its caller
+    {
+        ProfScope ps(cls(DASH_K_ROPE), st);
+        DASH_HIP(launch_rope_table(pos, w.cs, rows, d.head_dim, d.rope_theta, st));
+    }
+    for (int l = 0; l < d.n_layers; ++l) {
+        if (l > 0) {
+            ProfScope ps(cls(DASH_K_NORM), st);
+            DASH_HIP(launch_add_rmsnorm(dt, w.x, w.delta, sd, (size_t)rows * d.d_model, m->lw(l, 0), w.y, nullptr, rows,
+                                        d.d_model, d.rms_eps, 1, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_GEMM_QKV), st);
+            DASH_HIP(launch_gemm(dt, EPI_STORE_F32, w.y, m->lw(l, 1), w.qkv, rows, qr, d.d_model, qr, sq,
+                                 (size_t)rows * qr, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_ROPE), st);
+            DASH_HIP(launch_qkv_rope_append(dt, w.qkv, sq, (size_t)rows * qr, m->lw(l, 2), w.cs, pos, slot,
+                                            kv->d_table, kv->pool, kv->g, l, w.q, rows, d.n_heads, kv->d_status, st));
+        }
+        if (prefill) {
+            DASH_HIP(launch_prefill_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads, w.o, rows,
+                                              st));
+        } else {
+            {
+                ProfScope ps(DASH_K_ATTN, st);
+                DASH_HIP(launch_decode_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads, w.o,
+                                                 rows, kv->max_ctx, w.attn_part, st));
+            }
+            ProfScope ps(DASH_K_ATTN_COMBINE, st);
+            DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, w.attn_part, w.o, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_GEMM_O), st);
+            DASH_HIP(launch_gemm(dt, EPI_STORE_F32, w.o, m->lw(l, 3), w.delta, rows, d.d_model, hq, d.d_model, so,
+                                 (size_t)rows * d.d_model, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_NORM), st);
+            DASH_HIP(launch_add_rmsnorm(dt, w.x, w.delta, so, (size_t)rows * d.d_model, m->lw(l, 4), w.y, nullptr, rows,
+                                        d.d_model, d.rms_eps, 1, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_GEMM_GATE_UP), st);
+            DASH_HIP(launch_gemm(dt, EPI_SWIGLU, w.y, m->lw(l, 5), w.h, rows, 2 * d.d_ff, d.d_model, d.d_ff, 1, 0, st));
+        }
+        {
+            ProfScope ps(cls(DASH_K_GEMM_DOWN), st);
+            DASH_HIP(launch_gemm(dt, EPI_STORE_F32, w.h, m->lw(l, 6), w.delta, rows, d.d_model, d.d_ff, d.d_model, sd,
+                                 (size_t)rows * d.d_model, st));
+        }
+    }
+    *last_split = sd;
+    return DASH_OK;
+}
+
+int check_ws(const dash_model* m, void* ws, size_t ws_bytes, int rows, int max_ctx) {
+    if (!ws) return fail(DASH_EINVAL, "workspace is NULL");
+    if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
+    const size_t need = plan_ws(m, rows, nullptr, max_ctx).bytes;
+    if (ws_bytes < need) return fail(DASH_ECAPACITY, "workspace too small: %zu < %zu bytes for %d rows", ws_bytes, need, rows);
+    return DASH_OK;
+}
+
+int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32_t* slot, const int32_t* pos, int rows,
+                     float* logits, void* ws, hipStream_t st) {
+    const auto& d = m->d;
+    Ws w = plan_ws(m, rows, (char*)ws, kv->max_ctx);
+    {
+        ProfScope ps(DASH_K_EMBED, st);
+        DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab,
+                                      d.rms_eps, st));
+    }
+    int sd = 1;
+    int rc = run_layers(m, kv, w, rows, pos, slot, false, st, &sd);
+    if (rc) return rc;
+    {
+        ProfScope ps(DASH_K_NORM, st);
+        DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, nullptr,
+                                    rows, d.d_model, d.rms_eps, 1, st));
+    }
+    ProfScope ps(DASH_K_GEMM_LM_HEAD, st);
+    DASH_HIP(launch_gemm(d.dtype, EPI_STORE_F32, w.y, m->embed(), logits, rows, d.vocab, d.d_model, d.vocab, 1, 0, st));
+    return DASH_OK;
+}
+
+int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prompts, int P, int G,
+                 const int32_t* h_slots, float* d_logits, void* ws, size_t ws_bytes, hipStream_t st) {
+    const auto& d = m->d;
+    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    // capacity: full prompt pages once per prompt, one private partial page per sample
+    const int full = P / ps, part = P % ps ? 1 : 0;
+    const size_t need = (size_t)n_prompts * (full + (size_t)part * G);
+    if (need > kv->free_list.size())
+        return fail(DASH_ECAPACITY, "pool exhausted: prefill needs %zu pages, %zu free", need, kv->free_list.size());
+    const int rows_fit = ws_rows_for(m, ws_bytes, n_prompts * P);
+    const int chunk = rows_fit / P;
+    if (chunk < 1) return fail(DASH_ECAPACITY, "workspace cannot hold one prompt of %d tokens", P);
+    // host bookkeeping: pages of every sample's slot
+    std::vector<int32_t> pairs;
+    for (int p = 0; p < n_prompts; ++p) {
+        const int s0 = h_slots[p * G];
+        for (int j = 0; j < full + part; ++j) kv->table[(size_t)s0 * mp + j] = kv_alloc_page(kv);
+        kv->npages[s0] = full + part;
+        kv->len[s0] = P;
+        for (int g = 1; g < G; ++g) {
+            const int s = h_slots[p * G + g];
+            for (int j = 0; j < full; ++j) {
+                const int pg = kv->table[(size_t)s0 * mp + j];
+                kv->table[(size_t)s * mp + j] = pg;
+                kv->refc[pg]++;
+            }
+            if (part) {
+                const int pg = kv_alloc_page(kv);
+                kv->table[(size_t)s * mp + full] = pg;
+                pairs.push_back(kv->table[(size_t)s0 * mp + full]);
+                pairs.push_back(pg);
+            }
+            kv->npages[s] = full + part;
+            kv->len[s] = P;
+        }
+    }
+    int lo = kv->g.max_seqs, hi = -1;
+    for (int i = 0; i < n_prompts * G; ++i) {
+        lo = std::min(lo, h_slots[i]);
+        hi = std::max(hi, h_slots[i]);
+    }
+    int rc = kv_push_rows(kv, lo, hi, st);
+    if (rc) return rc;
+
+    Ws w = plan_ws(m, chunk * P, (char*)ws, 0);
+    for (int p0 = 0; p0 < n_prompts; p0 += chunk) {
+        const int np = std::min(chunk, n_prompts - p0);
+        const int rows = np * P;
+        std::vector<int32_t> pos(rows), slot(rows), gather(np);
+        for (int i = 0; i < rows; ++i) {
+            pos[i] = i % P;
+            slot[i] = h_slots[(p0 + i / P) * G];
+        }
+        for (int i = 0; i < np; ++i) gather[i] = i * P + P - 1;
+        if ((rc = kv_upload(kv, w.pos, pos.data(), rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.slot, slot.data(), rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.gather, gather.data(), np * 4, st))) return rc;
+        DASH_HIP(launch_embed_rmsnorm(d.dtype, d_tokens + (size_t)p0 * P, m->embed(), m->lw(0, 0), w.x, w.y, rows,
+                                      d.d_model, d.vocab, d.rms_eps, st));
+        int sd = 1;
+        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, st, &sd))) return rc;
+        // final norm of the last position of every prompt only
+        DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
+                                    np, d.d_model, d.rms_eps, 0, st));
+        DASH_HIP(launch_gemm(d.dtype, EPI_STORE_F32, w.y, m->embed(), d_logits + (size_t)p0 * d.vocab, np, d.vocab,
+                             d.d_model, d.vocab, 1, 0, st));
+    }
+    if (!pairs.empty()) {
+        const int n = (int)pairs.size() / 2;
+        for (int i0 = 0; i0 < n; i0 += chunk * P) {  // the pairs buffer holds rows-many pairs
+            const int c = std::min(n - i0, chunk * P);
+            if ((rc = kv_upload(kv, w.pairs, pairs.data() + 2 * i0, (size_t)c * 8, st))) return rc;
+            DASH_HIP(launch_copy_pages(d.dtype, kv->pool, kv->g, w.pairs, c, st));
+        }
+    }
+    return DASH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dash_prefill(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int32_t n_prompts, int32_t P, int32_t G,
+                 const int32_t* h_slots, float* d_logits, void* ws, size_t ws_bytes, void* stream) {
+    if (!m || !kv || !d_tokens || !h_slots || !d_logits) return fail(DASH_EINVAL, "dash_prefill: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (n_prompts < 1 || P < 1 || G < 1) return fail(DASH_EINVAL, "n_prompts, prompt_len and group must be >= 1");
+    if (P > kv->max_ctx) return fail(DASH_ECAPACITY, "prompt_len %d exceeds max_ctx %d", P, kv->max_ctx);
+    if ((int64_t)n_prompts * G > kv->g.max_seqs) return fail(DASH_ECAPACITY, "more samples than slots");
+    std::vector<char> seen(kv->g.max_seqs, 0);
+    for (int i = 0; i < n_prompts * G; ++i) {
+        const int s = h_slots[i];
+        if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
+        if (seen[s]) return fail(DASH_EINVAL, "slot %d listed twice", s);
+        seen[s] = 1;
+        if (kv->npages[s] || kv->len[s]) return fail(DASH_EINVAL, "slot %d is not empty", s);
+    }
+    if (!ws) return fail(DASH_EINVAL, "workspace is NULL");
+    if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
+    ProfScope ps(DASH_K_PREFILL, (hipStream_t)stream);
+    return prefill_impl(m, kv, d_tokens, n_prompts, P, G, h_slots, d_logits, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int dash_decode_step(dash_model* m, dash_kv* kv, const int32_t* tok, const int32_t* slot, const int32_t* pos,
+                     int32_t rows, float* logits, void* ws, size_t ws_bytes, void* stream) {
+    if (!m || !kv || !tok || !slot || !pos || !logits) return fail(DASH_EINVAL, "dash_decode_step: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (rows < 1) return fail(DASH_EINVAL, "n_rows must be >= 1");
+    int rc = check_ws(m, ws, ws_bytes, rows, kv->max_ctx);
+    if (rc) return rc;
+    return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream);
+}
+
+int dash_sample(const float* logits, int64_t ld, int32_t rows, int32_t vocab, const int32_t* row_of,
+                const int32_t* uid, const int32_t* step, float temperature, uint64_t seed, int32_t* tok_out,
+                float* lp_out, void* stream) {
+    if (!logits || !uid || !step || !tok_out) return fail(DASH_EINVAL, "dash_sample: NULL argument");
+    if (rows < 0 || vocab < 1 || ld < vocab) return fail(DASH_EINVAL, "dash_sample: bad sizes");
+    if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DASH_EINVAL, "temperature must be > 0 and finite");
+    if (rows == 0) return DASH_OK;
+    ProfScope ps(DASH_K_SAMPLE, (hipStream_t)stream);
+    DASH_HIP(launch_sample(logits, ld, rows, vocab, row_of, uid, step, temperature, seed, tok_out, lp_out, nullptr,
+                           nullptr, 0, (hipStream_t)stream));
+    return DASH_OK;
+}
+
+int dash_group_advantage_filter(const float* r, int32_t n_groups, int32_t group, int32_t mode, float eps, float tau,
+                                float* adv, int32_t* kept, int32_t* count, void* stream) {
+    if (!r || !adv || !kept || !count) return fail(DASH_EINVAL, "dash_group_advantage_filter: NULL argument");
+    if (n_groups < 1 || group < 1) return fail(DASH_EINVAL, "n_groups and group must be >= 1");
+    if (mode < DASH_ADV_MEAN_ONLY || mode > DASH_ADV_STD_SAMPLE) return fail(DASH_EINVAL, "bad mode %d", mode);
+    if (!(eps >= 0.f) || !(tau >= 0.f)) return fail(DASH_EINVAL, "eps and tau must be >= 0 (and not NaN)");
+    if (group > 1024) return fail(DASH_ENOTSUP, "group > 1024");
+    if ((int64_t)n_groups * group > (1 << 24)) return fail(DASH_ENOTSUP, "more than 2^24 samples");
+    ProfScope ps(DASH_K_ADVANTAGE, (hipStream_t)stream);
+    DASH_HIP(launch_group_advantage_filter(r, n_groups, group, mode, eps, tau, adv, kept, count, (hipStream_t)stream));
+    return DASH_OK;
+}
+
+int dash_live_compact(const int32_t* tok, const int32_t* slot, const int32_t* pos, const int32_t* step,
+                      const int32_t* uid, const int32_t* budget, int32_t eos_id, int32_t n, int32_t* tok_o,
+                      int32_t* slot_o, int32_t* pos_o, int32_t* step_o, int32_t* uid_o, int32_t* count, void* stream) {
+    if (!tok || !slot || !pos || !step || !uid || !budget || !tok_o || !slot_o || !pos_o || !step_o || !uid_o || !count)
+        return fail(DASH_EINVAL, "dash_live_compact: NULL argument");
+    if (n < 0) return fail(DASH_EINVAL, "n_rows must be >= 0");
+    DASH_HIP(launch_live_compact(tok, slot, pos, step, uid, budget, eos_id, n, tok_o, slot_o, pos_o, step_o, uid_o,
+                                 count, (hipStream_t)stream));
+    return DASH_OK;
+}
+
+// ------------------------------------------------------ rollout driver ----
+
+namespace {
+
+struct RolloutWs {
+    Ws step;
+    float* logits;
+    int32_t* st[2][5];  // tok, slot, pos, step, uid
+    int32_t* row_of;
+    int32_t* budget;
+    int32_t* count;
+    size_t bytes;
+};
+
+RolloutWs plan_rollout(const dash_model* m, int n_prompts, int P, int G, int max_ctx, char* base) {
+    const int N = n_prompts * G;
+    // prefill chunks of up to 64 prompts (rows = 64 P) unless the batch is smaller
+    const int prefill_rows = std::min(n_prompts, std::max(1, 16384 / std::max(1, P))) * P;
+    const int rows = std::max(N, prefill_rows);
+    RolloutWs r{};
+    r.step = plan_ws(m, rows, base, max_ctx);
+    size_t off = r.step.bytes;
+    auto take = [&](size_t bytes) {
+        char* p = base ? base + off : nullptr;
+        off = align_up(off + bytes, 256);
+        return p;
+    };
+    r.logits = (float*)take((size_t)std::max(N, n_prompts) * m->d.vocab * 4);
+    for (int b = 0; b < 2; ++b)
+        for (int i = 0; i < 5; ++i) r.st[b][i] = (int32_t*)take((size_t)N * 4);
+    r.row_of = (int32_t*)take((size_t)N * 4);
+    r.budget = (int32_t*)take((size_t)N * 4);
+    r.count = (int32_t*)take(256);
+    r.bytes = off;
+    return r;
+}
+
+}  // namespace
+
+size_t dash_rollout_workspace_bytes(const dash_model* m, int32_t n_prompts, int32_t P, int32_t G, int32_t max_ctx) {
+    if (!m || n_prompts < 1 || P < 1 || G < 1 || max_ctx < 1) return 0;
+    return plan_rollout(m, n_prompts, P, G, max_ctx, nullptr).bytes;
+}
+
+int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n_prompts, int32_t P, int32_t G,
+                 int32_t T, const int32_t* h_budget, float temperature, uint64_t seed, int32_t* d_out_tokens,
+                 float* d_out_lp, int32_t use_graph, void* ws, size_t ws_bytes, void* stream) {
+    if (!m || !kv || !d_prompts || !d_out_tokens || !ws) return fail(DASH_EINVAL, "dash_rollout: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (n_prompts < 1 || P < 1 || G < 1 || T < 1) return fail(DASH_EINVAL, "sizes must be >= 1");
+    if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DASH_EINVAL, "temperature must be > 0 and finite");
+    const int N = n_prompts * G;
+    if (N > kv->g.max_seqs) return fail(DASH_ECAPACITY, "kv has %d slots, rollout needs %d", kv->g.max_seqs, N);
+    if (P + T > kv->max_ctx) return fail(DASH_ECAPACITY, "prompt_len + gen_len exceeds max_ctx");
+    for (int s = 0; s < N; ++s)
+        if (kv->npages[s] || kv->len[s]) return fail(DASH_EINVAL, "kv slot %d is not empty", s);
+    std::vector<int32_t> budget(N, T);
+    if (h_budget)
+        for (int i = 0; i < N; ++i) {
+            if (h_budget[i] < 1 || h_budget[i] > T) return fail(DASH_EINVAL, "budget[%d] = %d outside [1, %d]", i, h_budget[i], T);
+            budget[i] = h_budget[i];
+        }
+    if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
+    RolloutWs rw = plan_rollout(m, n_prompts, P, G, kv->max_ctx, (char*)ws);
+    if (ws_bytes < rw.bytes) return fail(DASH_ECAPACITY, "rollout workspace too small: %zu < %zu", ws_bytes, rw.bytes);
+    // page budget: worst case with every page private except shared full prompt pages
+    {
+        const int ps = kv->g.page_size;
+        size_t need = (size_t)n_prompts * (P / ps);
+        for (int i = 0; i < N; ++i) need += (size_t)(P + budget[i] + ps - 1) / ps - P / ps;
+        if (need > kv->free_list.size())
+            return fail(DASH_ECAPACITY, "pool too small for this rollout: %zu pages needed, %zu free", need,
+                        kv->free_list.size());
+    }
+    hipStream_t st = (hipStream_t)stream;
+    const auto& d = m->d;
+    const int V = d.vocab;
+    const bool ragged = std::any_of(budget.begin(), budget.end(), [&](int b) { return b != T; });
+    const size_t step_ws_bytes = rw.step.bytes;
+
+    DASH_HIP(launch_fill_i32(d_out_tokens, -1, (size_t)N * T, st));
+    int rc;
+    if ((rc = kv_upload(kv, rw.budget, budget.data(), (size_t)N * 4, st))) return rc;
+    std::vector<int32_t> slots(N);
+    for (int i = 0; i < N; ++i) slots[i] = i;
+    // 1. prefill
+    {
+        ProfScope ps(DASH_K_PREFILL, st);
+        if ((rc = prefill_impl(m, kv, d_prompts, n_prompts, P, G, slots.data(), rw.logits, ws, step_ws_bytes, st)))
+            return rc;
+    }
+    // 2. first token of every sample from its prompt's logits row
+    int cur = 0;
+    int32_t** S = rw.st[cur];  // tok, slot, pos, step, uid
+    DASH_HIP(launch_rows_init(S[1], S[4], S[2], S[3], N, P - 1, 0, st));
+    DASH_HIP(launch_iota_div(rw.row_of, N, G, st));
+    DASH_HIP(launch_sample(rw.logits, V, N, V, rw.row_of, S[4], S[3], temperature, seed, S[0], nullptr, d_out_tokens,
+                           d_out_lp, T, st));
+    // live rows after each step are known on the host from the budgets
+    std::vector<int> live_after(T + 1, 0);  // rows live for step t (t >= 1): budget > t
+    for (int i = 0; i < N; ++i)
+        for (int t = 1; t < budget[i] && t <= T; ++t) live_after[t]++;
+    std::vector<std::vector<int32_t>> done_at(T + 1);  // samples whose last token is step t
+    for (int i = 0; i < N; ++i) done_at[budget[i] - 1].push_back(i);
+
+    auto advance = [&](int n_rows) -> int {
+        if (!ragged) {
+            DASH_HIP(launch_rows_advance(S[2], S[3], n_rows, st));
+            return DASH_OK;
+        }
+        int32_t** O = rw.st[cur ^ 1];
+        DASH_HIP(launch_live_compact(S[0], S[1], S[2], S[3], S[4], rw.budget, -1, n_rows, O[0], O[1], O[2], O[3], O[4],
+                                     rw.count, st));
+        cur ^= 1;
+        S = rw.st[cur];
+        return DASH_OK;
+    };
+    if ((rc = advance(N))) return rc;
+    if ((rc = dash_kv_release(kv, done_at[0].data(), (int)done_at[0].size()))) return rc;
+
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    const bool graphs = use_graph && !ragged && st != nullptr;
+    std::vector<int32_t> live_slots;
+    for (int t = 1; t < T; ++t) {
+        const int B = ragged ? live_after[t] : N;
+        if (B == 0) break;
+        // rows live at step t feed position P + t - 1: reserve pages covering it
+        const int need_len = P + t;
+        if ((need_len - 1) % kv->g.page_size == 0) {
+            live_slots.clear();
+            for (int i = 0; i < N; ++i)
+                if (budget[i] > t) live_slots.push_back(i);
+            // one page ahead, capped at the last position the sample will feed (P + budget - 2)
+            const int ahead = (need_len + kv->g.page_size - 1) / kv->g.page_size * kv->g.page_size;
+            for (int s : live_slots) kv_grow(kv, s, std::min(P + budget[s] - 1, ahead));
+            if ((rc = kv_push_rows(kv, live_slots.front(), live_slots.back(), st))) return rc;
+        }
+        if (graphs) {
+            if (!exec) {
+                DASH_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+                g_prof.capturing = true;
+                int rc2 = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st);
+                if (!rc2) {
+                    hipError_t e = launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
+                                                 d_out_tokens, d_out_lp, T, st);
+                    if (e == hipSuccess) e = launch_rows_advance(S[2], S[3], B, st);
+                    if (e != hipSuccess) rc2 = fail(DASH_EDEVICE, "launch during capture: %s", hipGetErrorString(e));
+                }
+                g_prof.capturing = false;
+                hipError_t e = hipStreamEndCapture(st, &graph);
+                if (rc2) {
+                    if (graph) (void)hipGraphDestroy(graph);
+                    return rc2;
+                }
+                if (e != hipSuccess) return fail(DASH_EDEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
+                e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+                if (e != hipSuccess) {
+                    (void)hipGraphDestroy(graph);
+                    return fail(DASH_EDEVICE, "hipGraphInstantiate: %s", hipGetErrorString(e));
+                }
+            }
+            DASH_HIP(hipGraphLaunch(exec, st));
+            continue;
+        }
+        if ((rc = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st))) return rc;
+        {
+            ProfScope ps(DASH_K_SAMPLE, st);
+            DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
+                                   d_out_tokens, d_out_lp, T, st));
+        }
+        {
+            ProfScope ps(DASH_K_OTHER, st);
+            if ((rc = advance(B))) return rc;
+        }
+        if (ragged && (rc = dash_kv_release(kv, done_at[t].data(), (int)done_at[t].size()))) return rc;
+    }
+    if (exec) (void)hipGraphExecDestroy(exec);
+    if (graph) (void)hipGraphDestroy(graph);
+    // release whatever is still held (fixed-length rollouts end with every slot live)
+    std::vector<int32_t> held;
+    for (int i = 0; i < N; ++i)
+        if (kv->npages[i]) held.push_back(i);
+    return dash_kv_release(kv, held.data(), (int)held.size());
+}
+
+}  // extern "C"

@@ -1,0 +1,128 @@
+// Vocab-wide temperature sampling: Gumbel-max with counter-based Philox noise.
+//
+// One workgroup of 256 threads per row.  Thread t walks vocab entries in groups
+// of four (one Philox call yields the noise of four consecutive entries) with a
+// stride of 256 groups, so a wave reads 1 KB of logits per step, coalesced.
+// Each thread keeps its best (score, index) and an online (max, sum of exp) for
+// the log-normaliser; waves merge with xor shuffles, then LDS merges the four
+// waves.  Ties in the score go to the smaller vocab index.  The kernel is ALU
+// bound (ten Philox rounds per four entries and two logs per entry), not HBM
+// bound.  Built with -ffp-contract=off: see sampler_math.h.
+#include "common.h"
+#include "kernels.h"
+#include "sampler_math.h"
+
+namespace dash {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+DASH_DEV bool better(float s, int i, float bs, int bi) { return s > bs || (s == bs && i < bi); }
+
+__global__ void __launch_bounds__(kThreads)
+sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ row_of,
+         const int32_t* __restrict__ uid, const int32_t* __restrict__ step, float temperature, uint32_t k0,
+         uint32_t k1, int32_t* __restrict__ tok_out, float* __restrict__ lp_out, int32_t* __restrict__ traj,
+         float* __restrict__ traj_lp, int traj_ld, int vec4) {
+    __shared__ float red_s[kThreads / 64];
+    __shared__ int red_i[kThreads / 64];
+    __shared__ float red_m[kThreads / 64];
+    __shared__ float red_z[kThreads / 64];
+    const int b = blockIdx.x;
+    const int r = row_of ? row_of[b] : b;
+    const float* row = logits + (int64_t)r * ld;
+    const uint32_t u_id = (uint32_t)uid[b], st = (uint32_t)step[b];
+    const bool unit_t = temperature == 1.0f;
+
+    float best_s = -INFINITY;
+    int best_i = 0x7FFFFFFF;
+    float mx = -INFINITY, z = 0.f;
+    const int n4 = (vocab + 3) >> 2;
+    for (int g = threadIdx.x; g < n4; g += kThreads) {
+        float l[4];
+        if (vec4 && 4 * g + 3 < vocab) {
+            const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
+            l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
+        }
+        const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, k0, k1);
+        const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (!isfinite(l[j])) continue;
+            const float sc = unit_t ? l[j] : div_rn(l[j], temperature);
+            const float s = sc + gumbel_from_bits(xs[j]);
+            if (s > best_s) {  // indices grow within a thread: strict > keeps the smallest on ties
+                best_s = s;
+                best_i = 4 * g + j;
+            }
+            if (sc > mx) {
+                z = z * __expf(mx - sc) + 1.0f;
+                mx = sc;
+            } else {
+                z += __expf(sc - mx);
+            }
+        }
+    }
+    // wave merge
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float os = __shfl_xor(best_s, o, 64);
+        const int oi = __shfl_xor(best_i, o, 64);
+        if (better(os, oi, best_s, best_i)) {
+            best_s = os;
+            best_i = oi;
+        }
+        const float om = __shfl_xor(mx, o, 64), oz = __shfl_xor(z, o, 64);
+        const float nm = fmaxf(mx, om);
+        z = (mx == -INFINITY ? 0.f : z * __expf(mx - nm)) + (om == -INFINITY ? 0.f : oz * __expf(om - nm));
+        mx = nm;
+    }
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red_s[w] = best_s;
+        red_i[w] = best_i;
+        red_m[w] = mx;
+        red_z[w] = z;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int i = 1; i < kThreads / 64; ++i) {
+        if (better(red_s[i], red_i[i], best_s, best_i)) {
+            best_s = red_s[i];
+            best_i = red_i[i];
+        }
+        const float nm = fmaxf(mx, red_m[i]);
+        z = (mx == -INFINITY ? 0.f : z * __expf(mx - nm)) + (red_m[i] == -INFINITY ? 0.f : red_z[i] * __expf(red_m[i] - nm));
+        mx = nm;
+    }
+    int tok = -1;
+    float lp = NAN;
+    if (best_i != 0x7FFFFFFF) {
+        tok = best_i;
+        const float sc = unit_t ? row[tok] : div_rn(row[tok], temperature);
+        lp = sc - mx - logf(z);
+    }
+    tok_out[b] = tok;
+    if (lp_out) lp_out[b] = lp;
+    if (traj) traj[(size_t)u_id * traj_ld + st] = tok;
+    if (traj_lp) traj_lp[(size_t)u_id * traj_ld + st] = lp;
+}
+
+}  // namespace
+
+hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
+                         const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
+                         int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,
+                         hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
+    sample_k<<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
+                                        (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
+    return hipGetLastError();
+}
+
+}  // namespace dash

@@ -1,0 +1,185 @@
+"""GPU parity of dash_prefill / dash_decode_step / dash_rollout against the oracle.
+
+For every generated position the GPU's logits are compared with the oracle's
+teacher-forced logits for the same tokens (max abs diff <= 1e-4 for float32
+shapes, <= 3e-2 for bfloat16 shapes), and the oracle sampler applied to the
+GPU's logits must reproduce the GPU's tokens bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as om
+from oracle import sampler as osm
+from paper_2505_17218_amd import _lib as L
+from paper_2505_17218_amd import engine, synth
+
+from gpu_util import dev_i32, make_kv, require_gpu, run_stepwise, shape_dict
+
+pytestmark = pytest.mark.gpu
+
+TOL = {synth.DT_F32: 1e-4, synth.DT_BF16: 3e-2}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+# bf16 shapes small enough for the oracle, covering both head dims, GQA groups
+# of 3/4/7, vocab tails (not a multiple of 128) and partial prompt pages.
+BF16_A = synth.Shape("bf16-hd64", 2, 256, 8, 2, 64, 512, 1000, 1e6, synth.DT_BF16)
+BF16_B = synth.Shape("bf16-hd128", 2, 384, 6, 2, 128, 768, 2051, 1e6, synth.DT_BF16)
+BF16_C = synth.Shape("bf16-gqa7", 1, 448, 7, 1, 64, 320, 700, 1e4, synth.DT_BF16)
+
+
+def _check_run(shape, w, prompts, G, T, run: "object", temp, seed, tol):
+    sd = shape_dict(shape)
+    N = prompts.shape[0] * G
+    worst = 0.0
+    for n in range(N):
+        ref = om.rollout_logits(sd, w, prompts[n // G], run.tokens[n])
+        err = np.abs(ref - run.logits[:, n, :]).max()
+        worst = max(worst, err)
+    assert worst <= tol, f"max |logits - oracle| = {worst}"
+    # the oracle sampler on the GPU's logits reproduces the GPU's tokens
+    for t in range(T):
+        want, want_lp = osm.sample(run.logits[t], np.arange(N), np.full(N, t), temp, seed)
+        np.testing.assert_array_equal(run.tokens[:, t], want)
+        np.testing.assert_allclose(run.logprobs[:, t], want_lp, atol=5e-5, rtol=2e-6)
+    return worst
+
+
+@pytest.mark.parametrize("page_size", [16, 7, 64])
+def test_tiny_fp32_stepwise_matches_oracle(page_size):
+    wl = synth.WORKLOADS["tiny"]
+    shape = wl.shape
+    w = synth.make_weights(shape, 0)
+    prompts = synth.make_prompts(wl, 0)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, page_size, wl.n_seqs, wl.prompt_len + wl.gen_len)
+    run = run_stepwise(model, kv, prompts, wl.group, wl.gen_len, wl.temperature, synth.sampler_seed(0))
+    worst = _check_run(shape, w, prompts, wl.group, wl.gen_len, run, wl.temperature, synth.sampler_seed(0),
+                       TOL[shape.dtype])
+    print(f"tiny fp32 ps={page_size}: max |dlogits| = {worst:.3g}")
+
+
+@pytest.mark.parametrize("shape,n_prompts,G,P,T", [
+    (BF16_A, 3, 4, 40, 40), (BF16_B, 2, 4, 64, 33), (BF16_C, 2, 2, 31, 20), (BF16_A, 1, 2, 600, 6)])
+def test_bf16_stepwise_matches_oracle(shape, n_prompts, G, P, T):
+    w = synth.make_weights(shape, 1)
+    wl = synth.Workload("t", shape, n_prompts, G, P, T)
+    prompts = synth.make_prompts(wl, 1)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, n_prompts * G, P + T)
+    run = run_stepwise(model, kv, prompts, G, T, 1.0, 77)
+    worst = _check_run(shape, w, prompts, G, T, run, 1.0, 77, TOL[shape.dtype])
+    print(f"{shape.name} P={P} T={T}: max |dlogits| = {worst:.3g}")
+
+
+def test_bf16_large_batch_gemm_tiles():
+    """160 decode rows (M > 128 with a tail) through the MFMA GEMMs; checked on sampled rows."""
+    shape = BF16_A
+    w = synth.make_weights(shape, 2)
+    wl = synth.Workload("t", shape, 40, 4, 20, 4)
+    prompts = synth.make_prompts(wl, 2)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, 160, 24)
+    run = run_stepwise(model, kv, prompts, 4, 4, 1.0, 5)
+    sd = shape_dict(shape)
+    for n in (0, 1, 63, 64, 127, 128, 129, 159):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], run.tokens[n])
+        assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype]
+
+
+def test_page_size_and_batch_invariance_bf16():
+    """Page size 32 vs 64 and a different batch composition give bit-identical tokens and logits."""
+    shape = BF16_B
+    w = synth.make_weights(shape, 3)
+    wl = synth.Workload("t", shape, 3, 2, 45, 12)
+    prompts = synth.make_prompts(wl, 3)
+    model = engine.Model(shape, w)
+    runs = []
+    for ps in (32, 64):
+        kv = make_kv(model, ps, 6, 64)
+        runs.append(run_stepwise(model, kv, prompts, 2, 12, 1.0, 8))
+    np.testing.assert_array_equal(runs[0].tokens, runs[1].tokens)
+    np.testing.assert_array_equal(runs[0].logits, runs[1].logits)
+    kv = make_kv(model, 32, 2, 64)
+    one = run_stepwise(model, kv, prompts[1:2], 2, 12, 1.0, 8)
+    # the same prompt in a smaller batch: the first-token logits are bit-identical
+    # (later steps differ because the sample ids, and so the noise, differ)
+    np.testing.assert_array_equal(one.logits[0], runs[0].logits[0][2:4])
+
+
+def test_rollout_driver_matches_stepwise_tiny():
+    wl = synth.WORKLOADS["tiny"]
+    w = synth.make_weights(wl.shape, 0)
+    prompts = synth.make_prompts(wl, 0)
+    model = engine.Model(wl.shape, w)
+    kv = make_kv(model, 16, wl.n_seqs, wl.prompt_len + wl.gen_len)
+    step = run_stepwise(model, kv, prompts, wl.group, wl.gen_len, 1.0, 2, keep_logits=False)
+    ro = engine.Rollout(model, kv, wl.n_prompts, wl.prompt_len, wl.group, wl.gen_len)
+    for use_graph in (False, True):
+        toks, lps = ro.run(dev_i32(prompts), 1.0, 2, use_graph=use_graph)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(toks.cpu().numpy(), step.tokens)
+        np.testing.assert_array_equal(lps.cpu().numpy(), step.logprobs)
+    assert kv.free_pages == kv.pool.numel() // L.dash_kv_page_bytes(model.handle, 16)
+
+
+@pytest.mark.parametrize("shape", [BF16_A, BF16_B])
+def test_rollout_driver_ragged_and_graph_bf16(shape):
+    w = synth.make_weights(shape, 4)
+    n_prompts, G, P, T = 4, 4, 37, 40
+    wl = synth.Workload("t", shape, n_prompts, G, P, T)
+    prompts = synth.make_prompts(wl, 4)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, n_prompts * G, P + T)
+    step = run_stepwise(model, kv, prompts, G, T, 1.0, 3)
+    ro = engine.Rollout(model, kv, n_prompts, P, G, T)
+    for use_graph in (False, True):
+        toks, lps = ro.run(dev_i32(prompts), 1.0, 3, use_graph=use_graph)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(toks.cpu().numpy(), step.tokens)
+    budgets = np.random.default_rng(0).integers(1, T + 1, n_prompts * G).astype(np.int32)
+    budgets[0], budgets[1] = 1, T
+    toks, lps = ro.run(dev_i32(prompts), 1.0, 3, budgets=budgets, use_graph=False)
+    torch.cuda.synchronize()
+    got = toks.cpu().numpy()
+    for n in range(n_prompts * G):
+        b = budgets[n]
+        # batch-invariant kernels: a sample's tokens do not depend on which other rows are live
+        np.testing.assert_array_equal(got[n, :b], step.tokens[n, :b])
+        assert (got[n, b:] == -1).all()
+    assert kv.free_pages == kv.pool.numel() // L.dash_kv_page_bytes(model.handle, 32)
+
+
+def test_capacity_errors():
+    shape = BF16_A
+    model = engine.Model(shape, synth.make_weights(shape, 0))
+    kv = engine.KVCache(model, 32, 4, 64, 3)
+    pr = dev_i32(np.zeros((2, 40)))
+    with pytest.raises(L.DashError) as e:  # 2 prompts x (1 full + 2 partial) pages > 3
+        engine.prefill(model, kv, pr, 2, [0, 1, 2, 3])
+    assert e.value.status == L.DASH_ECAPACITY
+    assert kv.free_pages == 3
+    with pytest.raises(L.DashError) as e:
+        L.dash_kv_reserve(kv.handle, [0], 65, engine.stream_handle())
+    assert e.value.status == L.DASH_ECAPACITY
+    ws = model.workspace(2, 64)
+    with pytest.raises(L.DashError) as e:
+        L.dash_decode_step(model.handle, kv.handle, pr.data_ptr(), pr.data_ptr(), pr.data_ptr(), 4, pr.data_ptr(),
+                           engine.aligned(ws), ws.numel() - 256, engine.stream_handle())
+    assert e.value.status == L.DASH_ECAPACITY
+
+
+def test_unbacked_position_sets_status_and_does_not_fault():
+    shape = BF16_A
+    model = engine.Model(shape, synth.make_weights(shape, 0))
+    kv = make_kv(model, 32, 2, 64)
+    L.dash_kv_reserve(kv.handle, [0], 10, engine.stream_handle())
+    logits = engine.decode_step(model, kv, dev_i32([1, 2]), dev_i32([0, 1]), dev_i32([5, 5]))
+    torch.cuda.synchronize()
+    assert torch.isfinite(logits[0]).all()
+    assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) & 1
+    assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) == 0

@@ -1,0 +1,124 @@
+"""GPU parity of dash_sample, dash_group_advantage_filter and dash_live_compact
+against the oracle (tokens, advantages and index sets bit-exact)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import advantage as oa
+from oracle import sampler as osm
+from paper_2505_17218_amd import _lib as L
+from paper_2505_17218_amd import engine, synth
+
+from gpu_util import dev_i32, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+# log-probability tolerance: fp32 online log-sum-exp over up to 151936 terms
+# (relative error of the sum ~1e-6) against the float64 oracle
+LP_ATOL, LP_RTOL = 5e-5, 2e-6
+
+
+@pytest.mark.parametrize("rows,vocab,temp,seed,scale", [
+    (16, 512, 1.0, 2, 1.0), (64, 151936, 1.0, 2, 2.0), (33, 151936, 0.7, 12345, 1.0),
+    (7, 5, 1.0, 3, 1.0), (5, 1, 1.0, 4, 1.0), (9, 1001, 2.5, 0xFFFFFFFFFFFF, 3.0), (1024, 4096, 1.0, 2, 1.0)])
+def test_sample_bitexact(rows, vocab, temp, seed, scale):
+    logits = synth.make_logits(rows, vocab, seed=rows + vocab, scale=scale)
+    rng = np.random.default_rng(vocab)
+    uid = rng.integers(0, 1 << 20, rows).astype(np.int32)
+    step = rng.integers(0, 2048, rows).astype(np.int32)
+    toks, lps = engine.sample(torch.from_numpy(logits).cuda(), dev_i32(uid), dev_i32(step), temp, seed)
+    want_t, want_lp = osm.sample(logits, uid, step, temp, seed)
+    np.testing.assert_array_equal(toks.cpu().numpy(), want_t)
+    np.testing.assert_allclose(lps.cpu().numpy(), want_lp, atol=LP_ATOL, rtol=LP_RTOL)
+
+
+def test_sample_row_of_stride_and_nonfinite():
+    V, R = 1000, 6
+    wide = synth.make_logits(R, V + 24, seed=9)  # row stride 1024 > vocab
+    wide[1, 17] = np.inf
+    wide[2, :V] = np.nan   # no finite logit: token -1
+    wide[3, 5] = np.nan
+    wide[4, 100:300] = -np.inf
+    dl = torch.from_numpy(wide).cuda()[:, :V]
+    row_of = np.array([0, 1, 3, 4, 5, 0, 1, 4], np.int32)
+    B = row_of.size
+    uid = np.arange(B, dtype=np.int32) * 7
+    step = np.full(B, 3, np.int32)
+    toks, lps = engine.sample(dl, dev_i32(uid), dev_i32(step), 1.0, 99, row_of=dev_i32(row_of))
+    want_t, want_lp = osm.sample(wide[:, :V], uid, step, 1.0, 99, row_of=row_of)
+    np.testing.assert_array_equal(toks.cpu().numpy(), want_t)
+    np.testing.assert_allclose(lps.cpu().numpy(), want_lp, atol=LP_ATOL, rtol=LP_RTOL)
+    toks2, _ = engine.sample(dl, dev_i32([0]), dev_i32([0]), 1.0, 1, row_of=dev_i32([2]))
+    assert int(toks2.item()) == -1
+
+
+def test_sample_deterministic_and_independent_of_batch_position():
+    logits = synth.make_logits(8, 151936, seed=5)
+    uid = np.arange(8, dtype=np.int32)
+    step = np.full(8, 10, np.int32)
+    a, _ = engine.sample(torch.from_numpy(logits).cuda(), dev_i32(uid), dev_i32(step), 1.0, 7)
+    perm = np.array([3, 1, 7, 0, 2, 6, 5, 4])
+    b, _ = engine.sample(torch.from_numpy(logits[perm]).cuda(), dev_i32(uid[perm]), dev_i32(step), 1.0, 7)
+    np.testing.assert_array_equal(a.cpu().numpy()[perm], b.cpu().numpy())
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 4, 5, 8, 16, 33, 64, 100, 1024])
+@pytest.mark.parametrize("mode", [L.DASH_ADV_MEAN_ONLY, L.DASH_ADV_STD_POP, L.DASH_ADV_STD_SAMPLE])
+def test_advantage_filter_bitexact(G, mode):
+    n_groups = max(1, 4096 // G)
+    r = synth.make_rewards(n_groups, G, "beta0.5", seed=G)
+    # mix in continuous rewards so |A| lands everywhere, including near tau
+    cont = np.random.default_rng(G).standard_normal(r.size).astype(np.float32) * np.float32(0.3)
+    for rr in (r, (r + cont).astype(np.float32)):
+        adv, kept = engine.advantage_filter(torch.from_numpy(rr).cuda(), G, mode, 1e-6, 0.1)
+        want = oa.group_advantage(rr, G, mode, 1e-6)
+        np.testing.assert_array_equal(adv.cpu().numpy().view(np.uint32), want.view(np.uint32))
+        np.testing.assert_array_equal(kept.cpu().numpy(), oa.gradient_filter(want, 0.1))
+
+
+@pytest.mark.parametrize("n_groups,G", [(4, 4), (128, 8), (512, 8), (8192, 8)])
+def test_advantage_workload_sizes(n_groups, G):
+    kind = "bernoulli0.5" if G == 4 else "beta0.5"
+    r = synth.make_rewards(n_groups, G, kind, seed=0)
+    adv, kept = engine.advantage_filter(torch.from_numpy(r).cuda(), G, L.DASH_ADV_STD_SAMPLE, 1e-6, 0.1)
+    want = oa.group_advantage(r, G, oa.STD_SAMPLE, 1e-6)
+    np.testing.assert_array_equal(adv.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    np.testing.assert_array_equal(kept.cpu().numpy(), oa.gradient_filter(want, 0.1))
+
+
+def test_advantage_tau_zero_and_tiny():
+    r = synth.make_rewards(64, 8, "beta0.5", seed=1)
+    d = torch.from_numpy(r).cuda()
+    _, kept0 = engine.advantage_filter(d, 8, L.DASH_ADV_MEAN_ONLY, 1e-6, 0.0)
+    assert kept0.numel() == r.size
+    _, kept1 = engine.advantage_filter(d, 8, L.DASH_ADV_MEAN_ONLY, 1e-6, float(np.finfo(np.float32).smallest_subnormal))
+    want = oa.gradient_filter(oa.group_advantage(r, 8, oa.MEAN_ONLY), np.finfo(np.float32).smallest_subnormal)
+    np.testing.assert_array_equal(kept1.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("n,eos", [(1, -1), (1000, -1), (4096, 7), (3000, -1)])
+def test_live_compact(n, eos):
+    rng = np.random.default_rng(n)
+    uid = rng.permutation(8192)[:n].astype(np.int32)
+    budget = rng.integers(1, 50, 8192).astype(np.int32)
+    step = rng.integers(0, 50, n).astype(np.int32)
+    tok = rng.integers(0, 16, n).astype(np.int32)
+    slot = rng.integers(0, 1 << 16, n).astype(np.int32)
+    pos = rng.integers(0, 4096, n).astype(np.int32)
+    outs = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in range(5)]
+    cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ins = [dev_i32(a) for a in (tok, slot, pos, step, uid)]
+    L.dash_live_compact(*[t.data_ptr() for t in ins], dev_i32(budget).data_ptr(), eos, n,
+                        *[t.data_ptr() for t in outs], cnt.data_ptr(), engine.stream_handle())
+    live = (step + 1 < budget[uid]) & ~((eos >= 0) & (tok == eos))
+    k = int(cnt.item())
+    assert k == live.sum()
+    got = [t.cpu().numpy()[:k] for t in outs]
+    for g, w in zip(got, (tok[live], slot[live], pos[live] + 1, step[live] + 1, uid[live])):
+        np.testing.assert_array_equal(g, w)
