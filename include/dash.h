@@ -122,7 +122,8 @@ int32_t dash_weight_count(const dash_model_desc* desc);
  *   +4 mlp_norm  [d_model]
  *   +5 w_gate_up [2 d_ff, d_model]                             rows: gate, then up
  *   +6 w_down    [d_model, d_ff]
- * Every pointer must be 16-byte aligned.  Shapes the kernels cover:
+ * Every pointer must be 16-byte aligned.  Shapes the kernels cover
+ * (d_model <= 4096 always):
  *   DASH_BF16: head_dim in {64, 128}, d_model % 64 == 0, d_ff % 64 == 0,
  *              n_heads / n_kv_heads <= 16;
  *   DASH_F32:  head_dim <= 128, d_model, d_ff multiples of 4.

@@ -15,8 +15,11 @@
 // denominators reduced once at the end.  Long contexts are split across
 // workgroups and merged by a second kernel in a fixed order (deterministic).
 //
-// Generic (fp32 caches, and prefill of any dtype): one wave per (row, query
-// head), scores with lanes over keys and the value sum with lanes over dims.
+// Prefill (bf16): the same MFMA block step with the 16 columns being 16
+// consecutive query positions of one head, masked causally per column.
+//
+// Generic (fp32 caches): one wave per (row, query head), scores with lanes over
+// keys and the value sum with lanes over dims.
 #include "common.h"
 #include "kernels.h"
 
@@ -28,6 +31,129 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// ---- shared MFMA block step ---------------------------------------------
+// A wave attends 16 "columns" (decode: the query heads of one GQA group;
+// prefill: 16 consecutive query positions of one head) to one block of 32 keys.
+
+template <int HD>
+struct KVRegs {
+    uint4 k[2][HD / 32];  // A operand of S^T = K Q^T: keys h*16 + (lane & 15), dims c*32 + (lane >> 4)*8 ..
+    uint4 v[HD / 16];     // A operand of O^T = V^T P^T: dims d*16 + (lane & 15), 8 permuted keys of lane group
+};
+
+// Load the block of 32 keys starting at key `kin` of a page (kin % 32 == 0).
+template <int HD>
+DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps, int kin, bool ok, int col, int grp) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int c = 0; c < HD / 32; ++c)
+            r.k[h][c] = ok ? *reinterpret_cast<const uint4*>(kb + ((size_t)c * ps + kin + h * 16 + col) * 32 + grp * 8)
+                           : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d)
+        r.v[d] = ok ? *reinterpret_cast<const uint4*>(vb + (size_t)(d * 16 + col) * ps + kin + grp * 8)
+                    : make_uint4(0, 0, 0, 0);
+}
+
+template <int HD>
+struct AttnState {
+    f32x4_t acc[HD / 16];  // acc[d][i] = O^T[dim d*16 + grp*4 + i][column]
+    float m, l;            // running max (log2 domain) and this lane's partial denominator
+};
+
+template <int HD>
+DASH_DEV void attn_init(AttnState<HD>& st) {
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) st.acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    st.m = -INFINITY;
+    st.l = 0.f;
+}
+
+// One block: keys key0 .. key0+31; this lane's column sees keys < lim; keys >= vlim
+// (wave-uniform) may hold stale data and have their V zeroed.
+template <int HD>
+DASH_DEV void attn_block(AttnState<HD>& st, KVRegs<HD>& r, const bf16x8_t (&qf)[HD / 32], int key0, int lim, int vlim,
+                         float scale_log2, int grp) {
+    f32x4_t s[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        s[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < HD / 32; ++c)
+            s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, r.k[h][c]), qf[c], s[h], 0, 0, 0);
+    }
+    // lane holds keys key0 + h*16 + grp*4 + i of its column
+    float t[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int key = key0 + h * 16 + grp * 4 + i;
+            const float v = key < lim ? s[h][i] * scale_log2 : -INFINITY;
+            t[h * 4 + i] = v;
+            mx = fmaxf(mx, v);
+        }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(st.m, mx);
+    // a column with no visible key yet keeps m = -inf: use 0 as the reference so no NaN appears
+    const float ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(st.m - ref);
+    st.m = m_new;
+    float psum = 0.f;
+    uint32_t pk[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float p0 = exp2f(t[2 * i] - ref), p1 = exp2f(t[2 * i + 1] - ref);
+        psum += p0 + p1;
+        pk[i] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+    }
+    st.l = st.l * alpha + psum;
+    const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+    if (key0 + 32 > vlim) {  // zero V of keys past the written context (0 * non-finite stale data = NaN)
+#pragma unroll
+        for (int d = 0; d < HD / 16; ++d) {
+            uint32_t w[4] = {r.v[d].x, r.v[d].y, r.v[d].z, r.v[d].w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int kk = j < 4 ? grp * 4 + j : 16 + grp * 4 + (j - 4);
+                if (key0 + kk >= vlim) w[j >> 1] &= (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+            }
+            r.v[d] = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+        st.acc[d] *= alpha;
+        st.acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, r.v[d]), pf, st.acc[d], 0, 0, 0);
+    }
+}
+
+// Sum the per-lane partial denominators of each column (lanes col, col+16, col+32, col+48).
+template <int HD>
+DASH_DEV float attn_denominator(const AttnState<HD>& st) {
+    float l = st.l;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    return l;
+}
+
+// Store the normalised column (4 consecutive dims per 16-dim block) as bf16.
+template <int HD>
+DASH_DEV void attn_store(const AttnState<HD>& st, float l, bf16_t* orow, int grp) {
+    const float inv = l > 0.f ? 1.0f / l : 0.f;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+        const uint32_t lo = (uint32_t)f2bf(st.acc[d][0] * inv) | ((uint32_t)f2bf(st.acc[d][1] * inv) << 16);
+        const uint32_t hi = (uint32_t)f2bf(st.acc[d][2] * inv) | ((uint32_t)f2bf(st.acc[d][3] * inv) << 16);
+        *reinterpret_cast<uint2*>(orow + d * 16 + grp * 4) = make_uint2(lo, hi);
+    }
+}
+
+// ---- decode ----------------------------------------------------------------
+
 template <int HD>
 __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
                                                          const int32_t* __restrict__ slot,
@@ -35,8 +161,8 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
                                                          const bf16_t* __restrict__ pool, KVGeom g, int layer,
                                                          int n_heads, bf16_t* __restrict__ o, int max_splits,
                                                          float* __restrict__ part, float scale_log2) {
-    constexpr int NC = HD / 32;  // 32-dim chunks (K-steps of the score MFMA)
-    constexpr int ND = HD / 16;  // 16-dim blocks of the output
+    constexpr int NC = HD / 32;
+    constexpr int ND = HD / 16;
     const int lane = threadIdx.x;
     const int n_kv = g.n_kv;
     const int row = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv, split = blockIdx.y;
@@ -61,120 +187,79 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
             qf[c] = __builtin_bit_cast(bf16x8_t, v);
         }
     }
-
-    f32x4_t acc[ND];
-#pragma unroll
-    for (int i = 0; i < ND; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
-
-    uint4 kr[2][NC], vr[ND];
-    auto load_block = [&](int b) {
+    AttnState<HD> st;
+    attn_init(st);
+    KVRegs<HD> r;
+    for (int b = b_begin; b < b_end; ++b) {
         const int key0 = b << 5;
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        const int kin = key0 % g.page_size;
-        const bf16_t* kb = pool + kv_block(g, layer, page, kvh, 0);
-        const bf16_t* vb = pool + kv_block(g, layer, page, kvh, 1);
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int c = 0; c < NC; ++c)
-                kr[h][c] = ok ? *reinterpret_cast<const uint4*>(kb + ((size_t)c * g.page_size + kin + h * 16 + head) * 32 +
-                                                                grp * 8)
-                              : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int d = 0; d < ND; ++d)
-            vr[d] = ok ? *reinterpret_cast<const uint4*>(vb + (size_t)(d * 16 + head) * g.page_size + kin + grp * 8)
-                       : make_uint4(0, 0, 0, 0);
-    };
-
-    for (int b = b_begin; b < b_end; ++b) {
-        load_block(b);
-        const int key0 = b << 5;
-        f32x4_t s[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            s[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int c = 0; c < NC; ++c)
-                s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[h][c]), qf[c], s[h],
-                                                               0, 0, 0);
-        }
-        // lane holds keys key0 + h*16 + grp*4 + r for head `head`
-        float t[8];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = key0 + h * 16 + grp * 4 + r;
-                const float v = key < ctx ? s[h][r] * scale_log2 : -INFINITY;
-                t[h * 4 + r] = v;
-                mx = fmaxf(mx, v);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = exp2f(m_run - m_new);
-        m_run = m_new;
-        float psum = 0.f;
-        uint32_t pk[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float p0 = exp2f(t[2 * i] - m_new), p1 = exp2f(t[2 * i + 1] - m_new);
-            psum += p0 + p1;
-            pk[i] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
-        }
-        l_run = l_run * alpha + psum;
-        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-        // Keys past the context have p = 0; zero their V too, so stale pool contents
-        // (possibly non-finite) cannot leak in through 0 * inf.
-        if (key0 + 32 > ctx) {
-#pragma unroll
-            for (int d = 0; d < ND; ++d) {
-                uint32_t w[4] = {vr[d].x, vr[d].y, vr[d].z, vr[d].w};
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int kk = j < 4 ? grp * 4 + j : 16 + grp * 4 + (j - 4);
-                    if (key0 + kk >= ctx) w[j >> 1] &= (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-                }
-                vr[d] = make_uint4(w[0], w[1], w[2], w[3]);
-            }
-        }
-#pragma unroll
-        for (int d = 0; d < ND; ++d) {
-            acc[d] *= alpha;
-            acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vr[d]), pf, acc[d], 0, 0, 0);
-        }
+        load_kv<HD>(r, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
+                    key0 % g.page_size, ok, head, grp);
+        attn_block<HD>(st, r, qf, key0, ctx, ctx, scale_log2, grp);
     }
-    l_run += __shfl_xor(l_run, 16, 64);
-    l_run += __shfl_xor(l_run, 32, 64);
-
-    // acc[d][r] = O^T[dim d*16 + grp*4 + r][head]
+    const float l = attn_denominator(st);
     if (head >= rep) return;
     const int qh = kvh * rep + head;
     if (nsplit == 1) {  // the only split: normalise and store
-        const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
-        bf16_t* orow = o + ((size_t)row * n_heads + qh) * HD;
-#pragma unroll
-        for (int d = 0; d < ND; ++d) {
-            const uint32_t lo = (uint32_t)f2bf(acc[d][0] * inv) | ((uint32_t)f2bf(acc[d][1] * inv) << 16);
-            const uint32_t hi = (uint32_t)f2bf(acc[d][2] * inv) | ((uint32_t)f2bf(acc[d][3] * inv) << 16);
-            *reinterpret_cast<uint2*>(orow + d * 16 + grp * 4) = make_uint2(lo, hi);
-        }
+        attn_store<HD>(st, l, o + ((size_t)row * n_heads + qh) * HD, grp);
     } else {
         const size_t base = ((size_t)row * n_heads + qh) * max_splits + split;
         float* op = part + base * HD;
 #pragma unroll
         for (int d = 0; d < ND; ++d)
-            *reinterpret_cast<float4*>(op + d * 16 + grp * 4) = make_float4(acc[d][0], acc[d][1], acc[d][2], acc[d][3]);
+            *reinterpret_cast<float4*>(op + d * 16 + grp * 4) =
+                make_float4(st.acc[d][0], st.acc[d][1], st.acc[d][2], st.acc[d][3]);
         if (grp == 0) {
             float* ml = part + (size_t)(gridDim.x / n_kv) * n_heads * max_splits * HD + base * 2;
-            ml[0] = m_run;
-            ml[1] = l_run;
+            ml[0] = st.m;
+            ml[1] = l;
         }
     }
+}
+
+// ---- prefill ---------------------------------------------------------------
+// One wave per (prompt, query head, 16 consecutive query positions), causal.
+// Rows of a prompt are contiguous: row = prompt * P + position.
+
+template <int HD>
+__global__ void __launch_bounds__(64) prefill_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ slot,
+                                                          const int32_t* __restrict__ page_table,
+                                                          const bf16_t* __restrict__ pool, KVGeom g, int layer,
+                                                          int n_heads, int P, bf16_t* __restrict__ o, float scale_log2) {
+    constexpr int NC = HD / 32;
+    const int lane = threadIdx.x, col = lane & 15, grp = lane >> 4;
+    const int qblocks = (P + 15) >> 4;
+    const int prompt = blockIdx.x / qblocks, q0 = (blockIdx.x % qblocks) * 16;
+    const int h = blockIdx.y, kvh = h / (n_heads / g.n_kv);
+    const int qp = q0 + col;                 // this column's query position
+    const bool valid = qp < P;
+    const int row = prompt * P + (valid ? qp : q0);
+    const int sl = slot[(size_t)prompt * P];
+    const int last = min(P, q0 + 16);        // keys < last are written
+    bf16x8_t qf[NC];
+    {
+        const bf16_t* qrow = q + ((size_t)row * n_heads + h) * HD;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) qf[c] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + c * 32 + grp * 8));
+    }
+    AttnState<HD> st;
+    attn_init(st);
+    KVRegs<HD> r;
+    const int lim = valid ? qp + 1 : 1;
+    const int nblk = (last + 31) >> 5;
+    for (int b = 0; b < nblk; ++b) {
+        const int key0 = b << 5;
+        int page = kv_page_of(g, page_table, sl, key0);
+        const bool ok = page >= 0;
+        page = ok ? page : 0;
+        load_kv<HD>(r, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
+                    key0 % g.page_size, ok, col, grp);
+        attn_block<HD>(st, r, qf, key0, lim, last, scale_log2, grp);
+    }
+    const float l = attn_denominator(st);
+    if (valid) attn_store<HD>(st, l, o + ((size_t)row * n_heads + h) * HD, grp);
 }
 
 // Merge the context splits of rows that have more than one, in split order:
@@ -303,9 +388,22 @@ hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int
 
 hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
                                     const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
-                                    int n_heads, void* o, int rows, hipStream_t st) {
+                                    int n_heads, void* o, int rows, int prompt_len, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     const float scale = 1.0f / sqrtf((float)g.head_dim);
+    if (dtype == 1 && prompt_len > 0 && rows % prompt_len == 0) {
+        dim3 grid((rows / prompt_len) * ((prompt_len + 15) / 16), n_heads);
+        const float sl2 = scale * kLog2e;
+        if (g.head_dim == 128)
+            prefill_attn_bf16_k<128><<<grid, 64, 0, st>>>((const bf16_t*)q, slot, page_table, (const bf16_t*)pool, g,
+                                                           layer, n_heads, prompt_len, (bf16_t*)o, sl2);
+        else if (g.head_dim == 64)
+            prefill_attn_bf16_k<64><<<grid, 64, 0, st>>>((const bf16_t*)q, slot, page_table, (const bf16_t*)pool, g,
+                                                          layer, n_heads, prompt_len, (bf16_t*)o, sl2);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     dim3 grid(rows, n_heads);
     if (dtype == 1)
         attn_generic_k<bf16_t><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool, g,

@@ -12,6 +12,7 @@ typedef uint16_t bf16_t;  // bfloat16 bit pattern
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 DASH_DEV float bf2f(bf16_t u) { return __uint_as_float(static_cast<uint32_t>(u) << 16); }
 

@@ -11,67 +11,108 @@ namespace {
 
 constexpr int kRowThreads = 256;
 
+// One wave per row, 4 rows per workgroup; a lane holds up to kMaxV float4 of
+// the row (d <= 64 * 4 * kMaxV), so the row is read once and reduced with
+// shuffles only.
+constexpr int kMaxV = 16;
+
+template <typename T>
+DASH_DEV void store4(T* p, float4 v);
+template <>
+DASH_DEV void store4<float>(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+template <>
+DASH_DEV void store4<bf16_t>(bf16_t* p, float4 v) {
+    const uint32_t lo = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+    const uint32_t hi = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+    *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+}
+template <typename T>
+DASH_DEV float4 load4(const T* p);
+template <>
+DASH_DEV float4 load4<float>(const float* p) { return *reinterpret_cast<const float4*>(p); }
+template <>
+DASH_DEV float4 load4<bf16_t>(const bf16_t* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xFFFF0000u));
+}
+
+DASH_DEV float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+DASH_DEV float dot4(float4 a) { return a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w; }
+
 // x[r] = E[tok[r]]; y[r] = RMSNorm(x[r]) * w.
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __restrict__ tok,
                                                                const T* __restrict__ E,
                                                                const T* __restrict__ w, float* __restrict__ x,
-                                                               T* __restrict__ y, int d, int vocab, float eps) {
-    __shared__ float red[16];
-    const int r = blockIdx.x;
+                                                               T* __restrict__ y, int rows, int d, int vocab,
+                                                               float eps) {
+    const int lane = threadIdx.x & 63;
+    const int r = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
+    if (r >= rows) return;
     int t = tok[r];
     t = t < 0 ? 0 : (t >= vocab ? vocab - 1 : t);  // never index outside the table
-    const T* e = E + (size_t)t * d;
-    float* xr = x + (size_t)r * d;
+    const int d4 = d >> 2;
+    float4 v[kMaxV];
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) {
-        const float v = ld_elem(e + i);
-        xr[i] = v;
-        ss += v * v;
+#pragma unroll
+    for (int j = 0; j < kMaxV; ++j) {
+        const int i = lane + 64 * j;
+        if (i < d4) {
+            v[j] = load4(E + (size_t)t * d + 4 * i);
+            ss += dot4(v[j]);
+        }
     }
-    ss = block_sum(ss, red);
+    ss = wave_sum(ss);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-    T* yr = y + (size_t)r * d;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) st_elem(yr + i, xr[i] * inv * ld_elem(w + i));
+#pragma unroll
+    for (int j = 0; j < kMaxV; ++j) {
+        const int i = lane + 64 * j;
+        if (i < d4) {
+            *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = v[j];
+            const float4 g = load4(w + 4 * i);
+            store4(y + (size_t)r * d + 4 * i, make_float4(v[j].x * inv * g.x, v[j].y * inv * g.y, v[j].z * inv * g.z,
+                                                          v[j].w * inv * g.w));
+        }
+    }
 }
 
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads) add_rmsnorm_k(float* __restrict__ x, const float* __restrict__ delta,
                                                              int nsplit, size_t split_stride,
                                                              const T* __restrict__ w, T* __restrict__ y,
-                                                             const int32_t* __restrict__ row_map, int d, float eps,
-                                                             int write_x) {
-    __shared__ float red[16];
-    const int i_out = blockIdx.x;
+                                                             const int32_t* __restrict__ row_map, int rows, int d,
+                                                             float eps, int write_x) {
+    const int lane = threadIdx.x & 63;
+    const int i_out = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
+    if (i_out >= rows) return;
     const int r = row_map ? row_map[i_out] : i_out;
-    float* xr = x + (size_t)r * d;
-    T* yr = y + (size_t)i_out * d;
-    // keep up to 8 values per thread in registers (d <= 2048); beyond that, re-read x
-    constexpr int kReg = 8;
-    float v_reg[kReg];
+    const int d4 = d >> 2;
+    float4 v[kMaxV];
     float ss = 0.f;
-    int j = 0;
-    for (int i = threadIdx.x; i < d; i += blockDim.x, ++j) {
-        float v = xr[i];
-        if (delta)
-            for (int s = 0; s < nsplit; ++s) v += delta[s * split_stride + (size_t)r * d + i];
-        if (write_x) xr[i] = v;
-        if (j < kReg) v_reg[j] = v;
-        ss += v * v;
-    }
-    ss = block_sum(ss, red);
-    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-    j = 0;
-    for (int i = threadIdx.x; i < d; i += blockDim.x, ++j) {
-        float v;
-        if (j < kReg) {
-            v = v_reg[j];
-        } else {
-            v = xr[i];
-            if (!write_x && delta)
-                for (int s = 0; s < nsplit; ++s) v += delta[s * split_stride + (size_t)r * d + i];
+#pragma unroll
+    for (int j = 0; j < kMaxV; ++j) {
+        const int i = lane + 64 * j;
+        if (i < d4) {
+            float4 a = *reinterpret_cast<const float4*>(x + (size_t)r * d + 4 * i);
+            if (delta)
+                for (int s = 0; s < nsplit; ++s)
+                    a = add4(a, *reinterpret_cast<const float4*>(delta + s * split_stride + (size_t)r * d + 4 * i));
+            v[j] = a;
+            ss += dot4(a);
         }
-        st_elem(yr + i, v * inv * ld_elem(w + i));
+    }
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < kMaxV; ++j) {
+        const int i = lane + 64 * j;
+        if (i < d4) {
+            if (write_x) *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = v[j];
+            const float4 g = load4(w + 4 * i);
+            store4(y + (size_t)i_out * d + 4 * i, make_float4(v[j].x * inv * g.x, v[j].y * inv * g.y,
+                                                              v[j].z * inv * g.z, v[j].w * inv * g.w));
+        }
     }
 }
 
@@ -86,6 +127,7 @@ __global__ void rope_table_k(const int32_t* __restrict__ pos, float* __restrict_
     cs[2 * (size_t)idx + 1] = (float)sin(a);
 }
 
+// grid (rows, ceil(items / 256)): one RoPE pair of q or k, or one v element, per thread.
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads)
 qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride, const T* __restrict__ bias,
@@ -96,10 +138,9 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
     const int hd = g.head_dim, half = hd >> 1, n_kv = g.n_kv;
     const int qkv_rows = (n_heads + 2 * n_kv) * hd;
     const float* row = qkv + (size_t)r * qkv_rows;
-    const float* c_s = cs + (size_t)r * half * 2;
     const int p = pos[r];
     const int page = kv_page_of(g, page_table, slot[r], p);
-    if (page < 0 && threadIdx.x == 0 && status) atomicOr(status, 1u);
+    if (page < 0 && blockIdx.y == 0 && threadIdx.x == 0 && status) atomicOr(status, 1u);
     const int key = p % g.page_size;
     auto val = [&](int j) {
         float v = row[j];
@@ -107,30 +148,29 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
         return v + ld_elem(bias + j);
     };
     const int n_rope = (n_heads + n_kv) * half;
-    const int n_items = n_rope + n_kv * hd;
-    for (int it = threadIdx.x; it < n_items; it += blockDim.x) {
-        if (it < n_rope) {
-            const int h = it / half, i = it - h * half;
-            const int j = h * hd + i;
-            const float a = val(j), b = val(j + half);
-            const float c = c_s[2 * i], s = c_s[2 * i + 1];
-            const float lo = a * c - b * s, hi = b * c + a * s;
-            if (h < n_heads) {
-                T* q = q_out + ((size_t)r * n_heads + h) * hd;
-                st_elem(q + i, lo);
-                st_elem(q + i + half, hi);
-            } else if (page >= 0) {
-                T* kb = pool + kv_block(g, layer, page, h - n_heads, 0);
-                st_elem(kb + k_index<T>(g, key, i), lo);
-                st_elem(kb + k_index<T>(g, key, i + half), hi);
-            }
+    const int it = blockIdx.y * blockDim.x + threadIdx.x;
+    if (it < n_rope) {
+        const int h = it / half, i = it - h * half;
+        const int j = h * hd + i;
+        const float a = val(j), b = val(j + half);
+        const float* c_s = cs + ((size_t)r * half + i) * 2;
+        const float c = c_s[0], s = c_s[1];
+        const float lo = a * c - b * s, hi = b * c + a * s;
+        if (h < n_heads) {
+            T* q = q_out + ((size_t)r * n_heads + h) * hd;
+            st_elem(q + i, lo);
+            st_elem(q + i + half, hi);
         } else if (page >= 0) {
-            const int jj = it - n_rope;
-            const int h = jj / hd, dd = jj - h * hd;
-            const float v = val((n_heads + n_kv) * hd + jj);
-            T* vb = pool + kv_block(g, layer, page, h, 1);
-            st_elem(vb + v_index<T>(g, key, dd), v);
+            T* kb = pool + kv_block(g, layer, page, h - n_heads, 0);
+            st_elem(kb + k_index<T>(g, key, i), lo);
+            st_elem(kb + k_index<T>(g, key, i + half), hi);
         }
+    } else if (it < n_rope + n_kv * hd && page >= 0) {
+        const int jj = it - n_rope;
+        const int h = jj / hd, dd = jj - h * hd;
+        const float v = val((n_heads + n_kv) * hd + jj);
+        T* vb = pool + kv_block(g, layer, page, h, 1);
+        st_elem(vb + v_index<T>(g, key, dd), v);
     }
 }
 
@@ -174,14 +214,16 @@ inline unsigned cdiv(size_t a, size_t b) { return (unsigned)((a + b - 1) / b); }
 }  // namespace
 
 hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, const void* w, float* x, void* y,
-                                  int rows, int d, int vocab, float eps, hipStream_t st) {
+                                int rows, int d, int vocab, float eps, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
+    if (d % 4 || d > 256 * kMaxV) return hipErrorInvalidValue;
+    const unsigned blocks = cdiv(rows, kRowThreads / 64);
     if (dtype == 1)
-        embed_rmsnorm_k<bf16_t><<<rows, kRowThreads, 0, st>>>(tok, (const bf16_t*)E, (const bf16_t*)w, x,
-                                                              (bf16_t*)y, d, vocab, eps);
+        embed_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(tok, (const bf16_t*)E, (const bf16_t*)w, x,
+                                                                (bf16_t*)y, rows, d, vocab, eps);
     else
-        embed_rmsnorm_k<float><<<rows, kRowThreads, 0, st>>>(tok, (const float*)E, (const float*)w, x, (float*)y,
-                                                             d, vocab, eps);
+        embed_rmsnorm_k<float><<<blocks, kRowThreads, 0, st>>>(tok, (const float*)E, (const float*)w, x, (float*)y,
+                                                               rows, d, vocab, eps);
     return hipGetLastError();
 }
 
@@ -189,12 +231,14 @@ hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nspli
                               const void* w, void* y, const int32_t* row_map, int rows, int d, float eps,
                               int write_x, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
+    if (d % 4 || d > 256 * kMaxV) return hipErrorInvalidValue;
+    const unsigned blocks = cdiv(rows, kRowThreads / 64);
     if (dtype == 1)
-        add_rmsnorm_k<bf16_t><<<rows, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const bf16_t*)w,
-                                                            (bf16_t*)y, row_map, d, eps, write_x);
+        add_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const bf16_t*)w,
+                                                              (bf16_t*)y, row_map, rows, d, eps, write_x);
     else
-        add_rmsnorm_k<float><<<rows, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const float*)w,
-                                                           (float*)y, row_map, d, eps, write_x);
+        add_rmsnorm_k<float><<<blocks, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const float*)w,
+                                                             (float*)y, row_map, rows, d, eps, write_x);
     return hipGetLastError();
 }
 
@@ -210,12 +254,14 @@ hipError_t launch_qkv_rope_append(int dtype, const float* qkv, int nsplit, size_
                                   const int32_t* page_table, void* pool, const KVGeom& g, int layer,
                                   void* q_out, int rows, int n_heads, uint32_t* status, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
+    const int items = (n_heads + g.n_kv) * (g.head_dim / 2) + g.n_kv * g.head_dim;
+    dim3 grid(rows, cdiv(items, kRowThreads));
     if (dtype == 1)
-        qkv_rope_append_k<bf16_t><<<rows, kRowThreads, 0, st>>>(qkv, nsplit, split_stride, (const bf16_t*)bias, cs,
+        qkv_rope_append_k<bf16_t><<<grid, kRowThreads, 0, st>>>(qkv, nsplit, split_stride, (const bf16_t*)bias, cs,
                                                                 pos, slot, page_table, (bf16_t*)pool, g, layer,
                                                                 (bf16_t*)q_out, n_heads, status);
     else
-        qkv_rope_append_k<float><<<rows, kRowThreads, 0, st>>>(qkv, nsplit, split_stride, (const float*)bias, cs,
+        qkv_rope_append_k<float><<<grid, kRowThreads, 0, st>>>(qkv, nsplit, split_stride, (const float*)bias, cs,
                                                                pos, slot, page_table, (float*)pool, g, layer,
                                                                (float*)q_out, n_heads, status);
     return hipGetLastError();

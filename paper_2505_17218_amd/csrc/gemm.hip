@@ -1,16 +1,18 @@
 // Projection GEMMs C = A[M,K] . W[N,K]^T (fp32 accumulation).
 //
-// bfloat16: MFMA v_mfma_f32_16x16x32_bf16 tiles.  A workgroup of 4 waves owns a
-// BM x BN output tile (2 x 2 waves, each (BM/2) x (BN/2)); K advances in steps
-// of 64 through a double-buffered LDS tile (rows padded to 72 elements so the
-// 16-byte fragment reads of 16 consecutive rows hit distinct banks).  While
-// one k-step is multiplied, the next one is already in flight from HBM into
-// registers.  Work items (split, m-tile, n-tile) are enumerated m-fastest and
-// dealt to XCDs in contiguous runs, so the blocks that share a weight tile run
-// on the same XCD and reuse it from that XCD's L2.
+// bfloat16: v_mfma_f32_32x32x16_bf16 tiles (on gfx950 this MFMA sustains about
+// twice the rate of 16x16x32: measured ~2.1 vs ~1.24 PFLOP/s with register-only
+// operands).  A workgroup of WGM x WGN waves owns a BM x BN output tile; K
+// advances in steps of 64 through a double-buffered LDS tile (row-major, rows
+// padded to 72 elements so fragment reads of 16 consecutive rows hit distinct
+// banks).  Operands are fetched with raw buffer loads (rows outside the operand
+// read as zeros, no branches), PD k-steps ahead of the multiply.  Work items
+// (split, m-tile, n-tile) are enumerated m-fastest and dealt to XCDs in
+// contiguous runs, so blocks that share a weight tile run on the same XCD and
+// reuse it from that XCD's L2.
 //
 // float32: a plain LDS-tiled VALU kernel (the fp32 shapes are tiny correctness
-// configurations; there is no fp32 MFMA rate worth chasing there).
+// configurations).
 //
 // Epilogues: fp32 store (with split-K partials that the consumer sums in a
 // fixed order, so results are deterministic) or SwiGLU, where the B tile pairs
@@ -27,8 +29,10 @@ namespace {
 
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
-constexpr int kThreads = 256;
 constexpr int kXcds = 8;
+// Fourth dword of a raw buffer resource on gfx9-family GPUs (stride 0, 32-bit data
+// format): loads past num_records return zeros.
+constexpr int kBufferDword3 = 0x00020000;
 
 DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -40,13 +44,23 @@ DASH_DEV int xcd_remap(int bid, int nb) {
     return x * q + (x < r ? x : r) + j;
 }
 
-template <int BM, int BN, int EPI>
-__global__ void __launch_bounds__(kThreads) gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
-                                                        void* __restrict__ C, int M, int N, int K, int ldc,
-                                                        int m_tiles, int n_tiles, int kps, size_t split_stride) {
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
-    constexpr int A_CH = BM * 8 / kThreads, B_CH = BN * 8 / kThreads;  // 16-byte chunks per thread
-    static_assert(A_CH >= 1 && B_CH >= 1, "tile too small");
+// On gfx950 the 32x32x16 bf16 MFMA sustains about twice the rate of 16x16x32
+// (measured: ~2.1 vs ~1.24 PFLOP/s with register-only operands), so the main
+// kernel uses 32 x 32 output blocks.  Operand layout (per 16-wide k-step): lane l
+// holds row (l % 32) and k (l / 32) * 8 .. +8; output register i of lane l is
+// row (i / 4) * 8 + (l / 32) * 4 + i % 4, column l % 32.
+// LDS tiles are row-major with rows padded to 72 elements (fragment reads of 16
+// consecutive rows hit distinct banks); global loads fill full 128-byte rows.
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
+__global__ void __launch_bounds__(64 * WGM * WGN)
+gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __restrict__ C, int M, int N, int K,
+             int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;  // 16-byte chunks per thread per k-step
+    static_assert(A_CH >= 1 && B_CH >= 1 && BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile / thread mismatch");
+    static_assert(TM >= 1 && TN >= 1, "wave tile smaller than one MFMA block");
+    static_assert(EPI != EPI_SWIGLU || TN % 2 == 0, "SwiGLU pairs gate/up blocks inside a wave");
     __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * kLdsStride];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * kLdsStride];
 
@@ -58,118 +72,121 @@ __global__ void __launch_bounds__(kThreads) gemm_bf16_k(const bf16_t* __restrict
     const int m0 = mt * BM;
     const int k_begin = split * kps;
     const int k_end = min(K, k_begin + kps);
-
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wr = wave / WGN, wc = wave % WGN;
 
-    // Global row pointers of this thread's chunks.
-    const bf16_t* a_ptr[A_CH];
-    int a_lds[A_CH], a_kc[A_CH];
-    bool a_ok[A_CH];
+    // Operands are read with buffer loads: a row outside the operand gets a byte
+    // offset past the buffer's extent, which the hardware returns as zeros, so the
+    // loads need no branches and the compiler keeps PD k-steps of them in flight.
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16_t*>(A), 0, (int)((size_t)M * K * 2), kBufferDword3);
+    const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16_t*>(W), 0, (int)((size_t)N * K * 2), kBufferDword3);
+    constexpr uint32_t kOut = 0x80000000u;
+    uint32_t a_off[A_CH];
+    int a_lds[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
-        const int idx = tid + i * kThreads, row = idx >> 3, kc = idx & 7;
+        const int idx = tid + i * NT, row = idx >> 3, kc = idx & 7;
         const int m = m0 + row;
-        a_ok[i] = m < M;
-        a_ptr[i] = A + (size_t)(a_ok[i] ? m : 0) * K + kc * 8;
+        a_off[i] = m < M ? (uint32_t)(((size_t)m * K + kc * 8) * 2) : kOut;
         a_lds[i] = row * kLdsStride + kc * 8;
-        a_kc[i] = kc * 8;
     }
-    const bf16_t* b_ptr[B_CH];
-    int b_lds[B_CH], b_kc[B_CH];
-    bool b_ok[B_CH];
+    uint32_t b_off[B_CH];
+    int b_lds[B_CH];
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
-        const int idx = tid + i * kThreads, row = idx >> 3, kc = idx & 7;
+        const int idx = tid + i * NT, row = idx >> 3, kc = idx & 7;
         int n;
         bool ok;
         if (EPI == EPI_SWIGLU) {
-            // tile row -> (wave column, gate/up half, offset); ff = N / 2 gate rows then ff up rows
+            // a wave's N range holds WN/2 gate rows then the WN/2 up rows of the same columns
             const int ff = N >> 1;
-            const int wcol = row / (BN / 2), rr = row % (BN / 2);
-            const int j = nt * (BN / 2) + wcol * (BN / 4) + (rr % (BN / 4));
+            const int wcol = row / WN, rr = row % WN;
+            const int j = nt * (BN / 2) + wcol * (WN / 2) + (rr % (WN / 2));
             ok = j < ff;
-            n = (rr < BN / 4) ? j : ff + j;
+            n = rr < WN / 2 ? j : ff + j;
         } else {
             n = nt * BN + row;
             ok = n < N;
         }
-        b_ok[i] = ok;
-        b_ptr[i] = W + (size_t)(ok ? n : 0) * K + kc * 8;
+        b_off[i] = ok ? (uint32_t)(((size_t)n * K + kc * 8) * 2) : kOut;
         b_lds[i] = row * kLdsStride + kc * 8;
-        b_kc[i] = kc * 8;
     }
 
-    f32x4_t acc[TM][TN];
+    f32x16_t acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    uint4 ra[A_CH], rb[B_CH];
-    auto load = [&](int k0) {
+    uint4 ra[PD][A_CH], rb[PD][B_CH];
+    auto load = [&](int st, int k0) {
+        const uint32_t kb = (uint32_t)k0 * 2;
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) {
-            const bool ok = a_ok[i] && (k0 + a_kc[i] < k_end);
-            ra[i] = ok ? *reinterpret_cast<const uint4*>(a_ptr[i] + k0) : make_uint4(0, 0, 0, 0);
-        }
+        for (int i = 0; i < A_CH; ++i)
+            ra[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsA, a_off[i] + kb, 0, 0));
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i) {
-            const bool ok = b_ok[i] && (k0 + b_kc[i] < k_end);
-            rb[i] = ok ? *reinterpret_cast<const uint4*>(b_ptr[i] + k0) : make_uint4(0, 0, 0, 0);
-        }
+        for (int i = 0; i < B_CH; ++i)
+            rb[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsW, b_off[i] + kb, 0, 0));
     };
-    auto store = [&](int buf) {
+    auto store = [&](int st, int buf) {
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<uint4*>(&As[buf][a_lds[i]]) = ra[i];
+        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<uint4*>(&As[buf][a_lds[i]]) = ra[st][i];
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i) *reinterpret_cast<uint4*>(&Bs[buf][b_lds[i]]) = rb[i];
+        for (int i = 0; i < B_CH; ++i) *reinterpret_cast<uint4*>(&Bs[buf][b_lds[i]]) = rb[st][i];
     };
-
-    const int n_k = (k_end - k_begin + kBK - 1) / kBK;
-    if (n_k > 0) {
-        load(k_begin);
-        store(0);
-    }
-    __syncthreads();
-    const int frag_row = lane & 15, frag_k = (lane >> 4) * 8;
-    for (int kt = 0; kt < n_k; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < n_k) load(k_begin + (kt + 1) * kBK);
+    const int frow = lane & 31, fk = (lane >> 5) * 8;
+    auto compute = [&](int buf) {
 #pragma unroll
-        for (int ks = 0; ks < kBK; ks += 32) {
+        for (int ks = 0; ks < kBK; ks += 16) {
             bf16x8_t af[TM], bfr[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                af[i] = *reinterpret_cast<const bf16x8_t*>(
-                    &As[buf][(wr * WM + i * 16 + frag_row) * kLdsStride + ks + frag_k]);
+                af[i] = *reinterpret_cast<const bf16x8_t*>(&As[buf][(wr * WM + i * 32 + frow) * kLdsStride + ks + fk]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(
-                    &Bs[buf][(wc * WN + j * 16 + frag_row) * kLdsStride + ks + frag_k]);
+                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][(wc * WN + j * 32 + frow) * kLdsStride + ks + fk]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
-        if (kt + 1 < n_k) store(buf ^ 1);
-        __syncthreads();
+    };
+
+    const int n_k = (k_end - k_begin + kBK - 1) / kBK;
+#pragma unroll
+    for (int p = 0; p < PD; ++p) load(p, k_begin + p * kBK);
+    store(0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < n_k; kt += PD) {
+#pragma unroll
+        for (int u = 0; u < PD; ++u) {
+            const int k = kt + u;
+            // register stage u held step k (already in LDS): refill it with step k + PD
+            load(u, k_begin + (k + PD) * kBK);
+            if (k < n_k) compute(k & 1);
+            if (k + 1 < n_k) store((u + 1) % PD, (k + 1) & 1);
+            __syncthreads();
+        }
     }
 
-    // Output fragment: acc[i][j][r] = C[row (lane>>4)*4 + r][col lane&15] of the 16x16 block (i, j).
-    const int out_r = (lane >> 4) * 4, out_c = lane & 15;
+    // acc[i][j][r]: row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j)
+    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
     if (EPI == EPI_STORE_F32) {
         float* Cp = reinterpret_cast<float*>(C) + split * split_stride;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int n = nt * BN + wc * WN + j * 16 + out_c;
+                const int n = nt * BN + wc * WN + j * 32 + ccol;
                 if (n >= N) continue;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = m0 + wr * WM + i * 16 + out_r + r;
+                for (int r = 0; r < 16; ++r) {
+                    const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
                     if (m < M) Cp[(size_t)m * ldc + n] = acc[i][j][r];
                 }
             }
@@ -180,15 +197,36 @@ __global__ void __launch_bounds__(kThreads) gemm_bf16_k(const bf16_t* __restrict
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN / 2; ++j) {
-                const int col = nt * (BN / 2) + wc * (BN / 4) + j * 16 + out_c;
+                const int col = nt * (BN / 2) + wc * (WN / 2) + j * 32 + ccol;
                 if (col >= ff) continue;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = m0 + wr * WM + i * 16 + out_r + r;
+                for (int r = 0; r < 16; ++r) {
+                    const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
                     if (m < M) H[(size_t)m * ldc + col] = f2bf(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
                 }
             }
     }
+}
+
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
+hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int nsplit,
+                     size_t split_stride, hipStream_t st) {
+    const int m_tiles = (M + BM - 1) / BM;
+    const int cols = EPI == EPI_SWIGLU ? N / 2 : N;
+    const int tn = EPI == EPI_SWIGLU ? BN / 2 : BN;
+    const int n_tiles = (cols + tn - 1) / tn;
+    int kps = K;
+    if (nsplit > 1) {
+        kps = (K + nsplit - 1) / nsplit;
+        kps = (kps + kBK - 1) / kBK * kBK;
+    }
+    if ((K + kps - 1) / kps != nsplit) return hipErrorInvalidValue;
+    // k-steps of 64 never straddle the end of K or of a split; byte offsets fit 31 bits
+    if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
+    const int blocks = m_tiles * n_tiles * nsplit;
+    gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI><<<blocks, 64 * WGM * WGN, 0, st>>>(
+        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride);
+    return hipGetLastError();
 }
 
 // fp32: 64 x 64 output tile per 256 threads (16 x 16, 4 x 4 each), BK = 16.
@@ -251,25 +289,6 @@ __global__ void __launch_bounds__(256) gemm_f32_k(const float* __restrict__ A, c
     }
 }
 
-template <int BM, int BN, int EPI>
-hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int nsplit,
-                    size_t split_stride, hipStream_t st) {
-    const int m_tiles = (M + BM - 1) / BM;
-    const int n_cols = EPI == EPI_SWIGLU ? N / 2 : N;
-    const int n_tiles = (n_cols + (EPI == EPI_SWIGLU ? BN / 2 : BN) - 1) / (EPI == EPI_SWIGLU ? BN / 2 : BN);
-    int kps = K;
-    if (nsplit > 1) {
-        kps = (K + nsplit - 1) / nsplit;
-        kps = (kps + kBK - 1) / kBK * kBK;
-    }
-    const int splits = (K + kps - 1) / kps;
-    if (splits != nsplit) return hipErrorInvalidValue;
-    const int blocks = m_tiles * n_tiles * splits;
-    gemm_bf16_k<BM, BN, EPI><<<blocks, kThreads, 0, st>>>((const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc,
-                                                          m_tiles, n_tiles, kps, split_stride);
-    return hipGetLastError();
-}
-
 }  // namespace
 
 // Split-K count as a function of the weight shape only (never of M), so that a
@@ -291,13 +310,18 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                        int nsplit, size_t split_stride, hipStream_t st) {
     if (M <= 0 || N <= 0) return hipSuccess;
     if (dtype == 1) {
+        // Tile choice may depend on M: every configuration accumulates each output
+        // element with the same chain of 32x32x16 MFMAs over k, so results do not.
         if (epi == EPI_SWIGLU) {
             if (nsplit != 1) return hipErrorInvalidValue;
-            return M <= 64 ? run_bf16<64, 128, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st)
-                           : run_bf16<128, 128, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+            return M <= 64 ? run_bf16<64, 256, 1, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st)
+                           : run_bf16<128, 128, 2, 2, 4, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
         }
-        return M <= 64 ? run_bf16<64, 128, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st)
-                       : run_bf16<128, 128, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (M <= 64)
+            return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (N >= 8192)
+            return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        return run_bf16<128, 256, 2, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
     }
     if (nsplit != 1) return hipErrorInvalidValue;
     if (epi == EPI_SWIGLU) {

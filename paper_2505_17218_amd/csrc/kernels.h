@@ -62,10 +62,12 @@ size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx
 // Second pass of decode attention: merge the splits of rows longer than one split (bf16 only).
 hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
                                     int max_ctx, const float* ws_part, void* o, hipStream_t st);
-// Causal attention of prefill rows (generic kernel; row r attends to 0..pos[r] of slot[r]).
+// Causal attention of prefill rows: rows are whole prompts of prompt_len positions, row
+// r = prompt * prompt_len + position, all rows of a prompt in slot[prompt * prompt_len].
+// bf16: MFMA kernel; fp32: generic kernel (row r attends to 0..pos[r] of slot[r]).
 hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
                                     const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
-                                    int n_heads, void* o, int rows, hipStream_t st);
+                                    int n_heads, void* o, int rows, int prompt_len, hipStream_t st);
 
 // ---- sampling / advantage (sampler.hip, advantage.hip) ----
 hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,

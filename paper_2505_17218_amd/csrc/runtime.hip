@@ -280,6 +280,7 @@ int dash_model_create(const dash_model_desc* d, const void* const* w, int32_t n_
     if (d->dtype != DASH_F32 && d->dtype != DASH_BF16) return fail(DASH_EINVAL, "dtype must be DASH_F32 or DASH_BF16");
     if (!(d->rope_theta > 0.f) || !(d->rms_eps >= 0.f)) return fail(DASH_EINVAL, "bad rope_theta or rms_eps");
     if (n_w != dash_weight_count(d)) return fail(DASH_EINVAL, "expected %d weight pointers, got %d", dash_weight_count(d), n_w);
+    if (d->d_model > 4096) return fail(DASH_ENOTSUP, "d_model > 4096");
     if (d->dtype == DASH_BF16) {
         if (d->head_dim != 64 && d->head_dim != 128) return fail(DASH_ENOTSUP, "bf16 head_dim must be 64 or 128");
         if (d->d_model % 64 || d->d_ff % 64) return fail(DASH_ENOTSUP, "bf16 d_model and d_ff must be multiples of 64");
@@ -508,7 +509,7 @@ int ws_rows_for(const dash_model* m, size_t ws_bytes, int want) {
 // Leaves x updated by the last layer's down projection in (x, delta split partials) and
 // returns the split count of the last delta via *last_split.
 int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t* pos, const int32_t* slot,
-               bool prefill, hipStream_t st, int* last_split) {
+               bool prefill, int prefill_len, hipStream_t st, int* last_split) {
     const auto& d = m->d;
     const int dt = d.dtype;
     const int qr = m->qkv_rows();
@@ -539,7 +540,7 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
         }
         if (prefill) {
             DASH_HIP(launch_prefill_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads, w.o, rows,
-                                              st));
+                                              prefill_len, st));
         } else {
             {
                 ProfScope ps(DASH_K_ATTN, st);
@@ -591,7 +592,7 @@ int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
                                       d.rms_eps, st));
     }
     int sd = 1;
-    int rc = run_layers(m, kv, w, rows, pos, slot, false, st, &sd);
+    int rc = run_layers(m, kv, w, rows, pos, slot, false, 0, st, &sd);
     if (rc) return rc;
     {
         ProfScope ps(DASH_K_NORM, st);
@@ -663,7 +664,7 @@ int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prom
         DASH_HIP(launch_embed_rmsnorm(d.dtype, d_tokens + (size_t)p0 * P, m->embed(), m->lw(0, 0), w.x, w.y, rows,
                                       d.d_model, d.vocab, d.rms_eps, st));
         int sd = 1;
-        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, st, &sd))) return rc;
+        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, P, st, &sd))) return rc;
         // final norm of the last position of every prompt only
         DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
                                     np, d.d_model, d.rms_eps, 0, st));
