@@ -226,6 +226,21 @@ int dash_decode_step(dash_model* model, dash_kv* kv, const int32_t* d_tokens, co
                      void* stream);
 
 /*
+ * dash_decode_step for a batch made of prefix-sharing groups (the G samples of a
+ * prompt after the group fork): rows d_group_off[i] .. d_group_off[i+1]-1 (int32
+ * device array of n_groups + 1 ascending offsets, the last equal to n_rows, each
+ * group at most group_size <= 8 rows) share their first shared_len positions, i.e.
+ * the same pages (shared_len a multiple of page_size, at most the prompt's full
+ * pages).  Decode attention then reads each shared page once per group instead of
+ * once per row.  Results are bit-identical to dash_decode_step.  DASH_ENOTSUP for
+ * group_size > 8; fp32 models run the ungrouped kernels.
+ */
+int dash_decode_step_grouped(dash_model* model, dash_kv* kv, const int32_t* d_tokens, const int32_t* d_slots,
+                             const int32_t* d_pos, int32_t n_rows, const int32_t* d_group_off, int32_t n_groups,
+                             int32_t group_size, int32_t shared_len, float* d_logits, void* d_ws, size_t ws_bytes,
+                             void* stream);
+
+/*
  * Temperature sampling by Gumbel-max with counter-based noise.
  * Row b reads float32 logits row r = d_row_of ? d_row_of[b] : b at
  * d_logits + r * ld, and draws token argmax_v (l_v / T + g_v) over finite l_v

@@ -30,6 +30,8 @@ namespace dash {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kMaxGroupWaves = 16;  // samples per group served by one workgroup  // raw buffer resource word 3 (gfx9 family): out-of-range reads give 0
 
 // ---- shared MFMA block step ---------------------------------------------
 // A wave attends 16 "columns" (decode: the query heads of one GQA group;
@@ -42,18 +44,24 @@ struct KVRegs {
 };
 
 // Load the block of 32 keys starting at key `kin` of a page (kin % 32 == 0).
+// Buffer loads over the page's K and V blocks: an unbacked page gets an empty
+// range and reads as zeros, so the loads carry no branch and the next block can
+// be in flight while the current one is multiplied.
 template <int HD>
 DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps, int kin, bool ok, int col, int grp) {
+    const int bytes = ok ? ps * HD * 2 : 0;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(kb), 0, bytes, kBufferDword3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(vb), 0, bytes, kBufferDword3);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int c = 0; c < HD / 32; ++c)
-            r.k[h][c] = ok ? *reinterpret_cast<const uint4*>(kb + ((size_t)c * ps + kin + h * 16 + col) * 32 + grp * 8)
-                           : make_uint4(0, 0, 0, 0);
+            r.k[h][c] = __builtin_bit_cast(
+                uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (((c * ps + kin + h * 16 + col) * 32 + grp * 8) * 2), 0, 0));
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d)
-        r.v[d] = ok ? *reinterpret_cast<const uint4*>(vb + (size_t)(d * 16 + col) * ps + kin + grp * 8)
-                    : make_uint4(0, 0, 0, 0);
+        r.v[d] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((d * 16 + col) * ps + kin + grp * 8) * 2, 0, 0));
 }
 
 template <int HD>
@@ -189,15 +197,23 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
     }
     AttnState<HD> st;
     attn_init(st);
-    KVRegs<HD> r;
-    for (int b = b_begin; b < b_end; ++b) {
+    // two register sets: block b + 1 is fetched while block b is multiplied
+    KVRegs<HD> r[2];
+    auto fetch = [&](KVRegs<HD>& dst, int b) {
         const int key0 = b << 5;
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        load_kv<HD>(r, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
+        load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
                     key0 % g.page_size, ok, head, grp);
-        attn_block<HD>(st, r, qf, key0, ctx, ctx, scale_log2, grp);
+    };
+    fetch(r[0], b_begin);
+    for (int b = b_begin; b < b_end; b += 2) {
+        fetch(r[1], min(b + 1, b_end - 1));
+        attn_block<HD>(st, r[0], qf, b << 5, ctx, ctx, scale_log2, grp);
+        if (b + 1 >= b_end) break;
+        fetch(r[0], min(b + 2, b_end - 1));
+        attn_block<HD>(st, r[1], qf, (b + 1) << 5, ctx, ctx, scale_log2, grp);
     }
     const float l = attn_denominator(st);
     if (head >= rep) return;
@@ -213,6 +229,163 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
                 make_float4(st.acc[d][0], st.acc[d][1], st.acc[d][2], st.acc[d][3]);
         if (grp == 0) {
             float* ml = part + (size_t)(gridDim.x / n_kv) * n_heads * max_splits * HD + base * 2;
+            ml[0] = st.m;
+            ml[1] = l;
+        }
+    }
+}
+
+// ---- decode, prefix-shared groups --------------------------------------------
+// The G samples of a prompt share the prompt's full pages (the group fork).  One
+// workgroup serves a whole group for one kv head and one context split: wave w
+// handles batch row off[g] + w.  Key blocks inside the shared prefix are fetched
+// once per workgroup (each wave loads a share of the block's 16-byte fragments,
+// staged through LDS in fragment order so every wave then reads whole fragments
+// with conflict-free 16-byte LDS reads); blocks past the prefix are streamed by
+// each wave from its own pages exactly as in the per-row kernel.  Per row the
+// blocks, the arithmetic and its order are those of decode_attn_bf16_k, so the
+// results are bit-identical to it.
+
+template <int HD, int NW>
+__global__ void __launch_bounds__(64 * NW)
+decode_attn_group_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
+                         const int32_t* __restrict__ slot, const int32_t* __restrict__ page_table,
+                         const bf16_t* __restrict__ pool, KVGeom g, int layer, int n_heads,
+                         const int32_t* __restrict__ group_off, int shared_len, bf16_t* __restrict__ o,
+                         int max_splits, float* __restrict__ part, float scale_log2) {
+    constexpr int NC = HD / 32, ND = HD / 16;
+    constexpr int NF = 2 * NC + ND;  // 1 KB fragments per 32-key block (K halves x chunks, then V blocks)
+    __shared__ uint4 lds[2][NF * 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int n_kv = g.n_kv;
+    const int grp_id = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv, split = blockIdx.y;
+    const int r0 = group_off[grp_id], r1 = group_off[grp_id + 1];
+    const bool active = w < r1 - r0;
+    const int row = active ? r0 + w : r0;
+    const int rep = n_heads / n_kv;
+    const int head = lane & 15, grp = lane >> 4;
+    const int ctx = pos[row] + 1;
+    // the workgroup walks the blocks of its longest row; shorter rows mask the rest
+    int ctx_max = 0;
+    for (int i = r0; i < r1; ++i) ctx_max = max(ctx_max, pos[i] + 1);
+    constexpr int per = kAttnSplitKeys / 32;
+    const int nblk_wg = (ctx_max + 31) >> 5;
+    const int nsplit_wg = min((nblk_wg + per - 1) / per, max_splits);
+    if (split >= nsplit_wg) return;  // uniform over the workgroup
+    const int nblk = (ctx + 31) >> 5;
+    const int nsplit = min((nblk + per - 1) / per, max_splits);
+    const int b_begin = split * per;
+    const int b_end_wg = min(nblk_wg, b_begin + per);
+    const int b_end = min(nblk, b_begin + per);
+    const int sh_blocks = min(shared_len >> 5, b_end_wg);  // blocks [0, sh_blocks) are shared
+    const int sl0 = slot[r0], sl = slot[row];
+
+    bf16x8_t qf[NC];
+    {
+        const bf16_t* qrow = q + ((size_t)row * n_heads + kvh * rep + (head < rep ? head : 0)) * HD;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            uint4 v = head < rep ? *reinterpret_cast<const uint4*>(qrow + c * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+            qf[c] = __builtin_bit_cast(bf16x8_t, v);
+        }
+    }
+    AttnState<HD> st;
+    attn_init(st);
+
+    // ---- shared blocks: cooperative fetch through LDS (all waves take part) ----
+    const int bs0 = b_begin, bs1 = min(sh_blocks, b_end_wg);
+    if (bs0 < bs1) {
+        // fragment f of block b: f < 2*NC is K (half f / NC, chunk f % NC), else V block f - 2*NC
+        auto frag_load = [&](int b, int f) -> uint4 {
+            const int key0 = b << 5;
+            int page = kv_page_of(g, page_table, sl0, key0);
+            const bool ok = page >= 0;
+            page = ok ? page : 0;
+            const int kin = key0 % g.page_size;
+            const int bytes = ok ? g.page_size * HD * 2 : 0;
+            if (f < 2 * NC) {
+                const int h = f / NC, c = f % NC;
+                const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, 0)), 0, bytes, kBufferDword3);
+                return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                    rk, (((c * g.page_size + kin + h * 16 + head) * 32 + grp * 8) * 2), 0, 0));
+            }
+            const int d = f - 2 * NC;
+            const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, 1)), 0, bytes, kBufferDword3);
+            return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                rv, ((d * 16 + head) * g.page_size + kin + grp * 8) * 2, 0, 0));
+        };
+        constexpr int FPW = (NF + NW - 1) / NW;  // fragments per wave
+        uint4 stage[FPW];
+        auto fetch = [&](int b) {
+#pragma unroll
+            for (int i = 0; i < FPW; ++i)
+                if (w + i * NW < NF) stage[i] = frag_load(b, w + i * NW);
+        };
+        auto put = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < FPW; ++i)
+                if (w + i * NW < NF) lds[buf][(w + i * NW) * 64 + lane] = stage[i];
+        };
+        fetch(bs0);
+        put(0);
+        __syncthreads();
+        for (int b = bs0; b < bs1; ++b) {
+            const int buf = (b - bs0) & 1;
+            fetch(min(b + 1, bs1 - 1));
+            if (active && b < b_end) {
+                KVRegs<HD> r;
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) r.k[h][c] = lds[buf][(h * NC + c) * 64 + lane];
+#pragma unroll
+                for (int d = 0; d < ND; ++d) r.v[d] = lds[buf][(2 * NC + d) * 64 + lane];
+                attn_block<HD>(st, r, qf, b << 5, ctx, ctx, scale_log2, grp);
+            }
+            if (b + 1 < bs1) put(buf ^ 1);
+            __syncthreads();
+        }
+    }
+
+    // ---- private blocks: each wave streams its own row ----
+    if (active) {
+        const int bp0 = max(b_begin, bs1);
+        if (bp0 < b_end) {
+            KVRegs<HD> r[2];
+            auto fetch = [&](KVRegs<HD>& dst, int b) {
+                const int key0 = b << 5;
+                int page = kv_page_of(g, page_table, sl, key0);
+                const bool ok = page >= 0;
+                page = ok ? page : 0;
+                load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1),
+                            g.page_size, key0 % g.page_size, ok, head, grp);
+            };
+            fetch(r[0], bp0);
+            for (int b = bp0; b < b_end; b += 2) {
+                fetch(r[1], min(b + 1, b_end - 1));
+                attn_block<HD>(st, r[0], qf, b << 5, ctx, ctx, scale_log2, grp);
+                if (b + 1 >= b_end) break;
+                fetch(r[0], min(b + 2, b_end - 1));
+                attn_block<HD>(st, r[1], qf, (b + 1) << 5, ctx, ctx, scale_log2, grp);
+            }
+        }
+    }
+    const float l = attn_denominator(st);
+    if (!active || head >= rep || split >= nsplit) return;
+    const int qh = kvh * rep + head;
+    if (nsplit == 1) {
+        attn_store<HD>(st, l, o + ((size_t)row * n_heads + qh) * HD, grp);
+    } else {
+        const size_t base = ((size_t)row * n_heads + qh) * max_splits + split;
+        float* op = part + base * HD;
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+            *reinterpret_cast<float4*>(op + d * 16 + grp * 4) =
+                make_float4(st.acc[d][0], st.acc[d][1], st.acc[d][2], st.acc[d][3]);
+        if (grp == 0) {
+            float* ml = part + (size_t)group_off[gridDim.x / n_kv] * n_heads * max_splits * HD + base * 2;
             ml[0] = st.m;
             ml[1] = l;
         }
@@ -246,17 +419,24 @@ __global__ void __launch_bounds__(64) prefill_attn_bf16_k(const bf16_t* __restri
     }
     AttnState<HD> st;
     attn_init(st);
-    KVRegs<HD> r;
     const int lim = valid ? qp + 1 : 1;
     const int nblk = (last + 31) >> 5;
-    for (int b = 0; b < nblk; ++b) {
+    KVRegs<HD> r[2];
+    auto fetch = [&](KVRegs<HD>& dst, int b) {
         const int key0 = b << 5;
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        load_kv<HD>(r, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
+        load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
                     key0 % g.page_size, ok, col, grp);
-        attn_block<HD>(st, r, qf, key0, lim, last, scale_log2, grp);
+    };
+    fetch(r[0], 0);
+    for (int b = 0; b < nblk; b += 2) {
+        fetch(r[1], min(b + 1, nblk - 1));
+        attn_block<HD>(st, r[0], qf, b << 5, lim, last, scale_log2, grp);
+        if (b + 1 >= nblk) break;
+        fetch(r[0], min(b + 2, nblk - 1));
+        attn_block<HD>(st, r[1], qf, (b + 1) << 5, lim, last, scale_log2, grp);
     }
     const float l = attn_denominator(st);
     if (valid) attn_store<HD>(st, l, o + ((size_t)row * n_heads + h) * HD, grp);
@@ -375,6 +555,36 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
     dim3 grid(rows, n_heads);
     attn_generic_k<float><<<grid, 64, 0, st>>>((const float*)q, pos, slot, page_table, (const float*)pool, g, layer,
                                                n_heads, (float*)o, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, const int32_t* slot,
+                                           const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                           int n_heads, const int32_t* group_off, int n_groups, int group_size,
+                                           int shared_len, void* o, int rows, int max_ctx, float* ws_part,
+                                           hipStream_t st) {
+    if (rows <= 0 || n_groups <= 0) return hipSuccess;
+    if (group_size < 1 || group_size > kMaxGroupWaves) return hipErrorInvalidValue;
+    const float sl2 = kLog2e / sqrtf((float)g.head_dim);
+    const int ms = std::max(1, (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys);
+    dim3 grid(n_groups * g.n_kv, ms);
+    const int nw = group_size <= 4 ? 4 : (group_size <= 8 ? 8 : 16);
+#define DASH_GROUP_LAUNCH(HDV, NWV)                                                                              \
+    decode_attn_group_bf16_k<HDV, NWV><<<grid, 64 * NWV, 0, st>>>((const bf16_t*)q, pos, slot, page_table,       \
+                                                                  (const bf16_t*)pool, g, layer, n_heads, group_off, \
+                                                                  shared_len, (bf16_t*)o, ms, ws_part, sl2)
+    if (g.head_dim == 128) {
+        if (nw == 4) DASH_GROUP_LAUNCH(128, 4);
+        else if (nw == 8) DASH_GROUP_LAUNCH(128, 8);
+        else DASH_GROUP_LAUNCH(128, 16);
+    } else if (g.head_dim == 64) {
+        if (nw == 4) DASH_GROUP_LAUNCH(64, 4);
+        else if (nw == 8) DASH_GROUP_LAUNCH(64, 8);
+        else DASH_GROUP_LAUNCH(64, 16);
+    } else {
+        return hipErrorInvalidValue;
+    }
+#undef DASH_GROUP_LAUNCH
     return hipGetLastError();
 }
 

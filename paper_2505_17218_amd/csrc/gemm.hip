@@ -315,13 +315,15 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
         if (epi == EPI_SWIGLU) {
             if (nsplit != 1) return hipErrorInvalidValue;
             return M <= 64 ? run_bf16<64, 256, 1, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st)
-                           : run_bf16<128, 128, 2, 2, 4, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+                           : run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
         }
         if (M <= 64)
             return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
-        if (N >= 8192)
-            return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
-        return run_bf16<128, 256, 2, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (N >= 8192)  // LM head: many tiles, the largest tile wins
+            return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (K >= 4096)
+            return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        return run_bf16<128, 128, 4, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
     }
     if (nsplit != 1) return hipErrorInvalidValue;
     if (epi == EPI_SWIGLU) {

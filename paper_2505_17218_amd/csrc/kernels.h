@@ -59,6 +59,15 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
                                    const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                    int n_heads, void* o, int rows, int max_ctx, float* ws_part, hipStream_t st);
 size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx);
+// Decode attention for batches made of groups of rows that share a prefix: rows
+// [group_off[i], group_off[i+1]) (at most group_size <= 16 of them) share their first
+// shared_len positions (the same pages, read from the group's first row).  Same
+// results as launch_decode_attention, bit for bit; bf16 only.
+hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, const int32_t* slot,
+                                           const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
+                                           int n_heads, const int32_t* group_off, int n_groups, int group_size,
+                                           int shared_len, void* o, int rows, int max_ctx, float* ws_part,
+                                           hipStream_t st);
 // Second pass of decode attention: merge the splits of rows longer than one split (bf16 only).
 hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
                                     int max_ctx, const float* ws_part, void* o, hipStream_t st);

@@ -45,6 +45,8 @@ int fail(int status, const char* fmt, ...) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+constexpr int kMaxGroupRows = 8;  // rows per prefix-shared group the grouped kernel serves
+
 // ------------------------------------------------------------- profiler ----
 // Event pairs around launches, by kernel class; a ring of pairs is harvested
 // lazily (a pair is read back only when its slot is reused or on read-out).
@@ -504,12 +506,19 @@ int ws_rows_for(const dash_model* m, size_t ws_bytes, int want) {
     return lo;
 }
 
+// Rows grouped by shared prefix (decode only): rows [off[i], off[i+1]) share
+// their first shared_len positions; group_size bounds the rows per group.
+struct GroupInfo {
+    const int32_t* off;
+    int n_groups, group_size, shared_len;
+};
+
 // Transformer body over `rows` rows whose x/y are already set (x fp32, y = RMSNorm(x) * attn_norm[0]).
 // prefill: attention via the generic causal kernel over the rows' own slots; decode: MFMA paged kernel.
 // Leaves x updated by the last layer's down projection in (x, delta split partials) and
 // returns the split count of the last delta via *last_split.
 int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t* pos, const int32_t* slot,
-               bool prefill, int prefill_len, hipStream_t st, int* last_split) {
+               bool prefill, int prefill_len, hipStream_t st, int* last_split, const GroupInfo* gi) {
     const auto& d = m->d;
     const int dt = d.dtype;
     const int qr = m->qkv_rows();
@@ -544,8 +553,13 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
         } else {
             {
                 ProfScope ps(DASH_K_ATTN, st);
-                DASH_HIP(launch_decode_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads, w.o,
-                                                 rows, kv->max_ctx, w.attn_part, st));
+                if (gi)
+                    DASH_HIP(launch_decode_attention_grouped(w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads,
+                                                             gi->off, gi->n_groups, gi->group_size, gi->shared_len,
+                                                             w.o, rows, kv->max_ctx, w.attn_part, st));
+                else
+                    DASH_HIP(launch_decode_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads,
+                                                     w.o, rows, kv->max_ctx, w.attn_part, st));
             }
             ProfScope ps(DASH_K_ATTN_COMBINE, st);
             DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, w.attn_part, w.o, st));
@@ -583,7 +597,7 @@ int check_ws(const dash_model* m, void* ws, size_t ws_bytes, int rows, int max_c
 }
 
 int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32_t* slot, const int32_t* pos, int rows,
-                     float* logits, void* ws, hipStream_t st) {
+                     float* logits, void* ws, hipStream_t st, const GroupInfo* gi = nullptr) {
     const auto& d = m->d;
     Ws w = plan_ws(m, rows, (char*)ws, kv->max_ctx);
     {
@@ -592,7 +606,7 @@ int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
                                       d.rms_eps, st));
     }
     int sd = 1;
-    int rc = run_layers(m, kv, w, rows, pos, slot, false, 0, st, &sd);
+    int rc = run_layers(m, kv, w, rows, pos, slot, false, 0, st, &sd, gi);
     if (rc) return rc;
     {
         ProfScope ps(DASH_K_NORM, st);
@@ -664,7 +678,7 @@ int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prom
         DASH_HIP(launch_embed_rmsnorm(d.dtype, d_tokens + (size_t)p0 * P, m->embed(), m->lw(0, 0), w.x, w.y, rows,
                                       d.d_model, d.vocab, d.rms_eps, st));
         int sd = 1;
-        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, P, st, &sd))) return rc;
+        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, P, st, &sd, nullptr))) return rc;
         // final norm of the last position of every prompt only
         DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
                                     np, d.d_model, d.rms_eps, 0, st));
@@ -717,6 +731,23 @@ int dash_decode_step(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
     return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream);
 }
 
+int dash_decode_step_grouped(dash_model* m, dash_kv* kv, const int32_t* tok, const int32_t* slot, const int32_t* pos,
+                             int32_t rows, const int32_t* d_group_off, int32_t n_groups, int32_t group_size,
+                             int32_t shared_len, float* logits, void* ws, size_t ws_bytes, void* stream) {
+    if (!m || !kv || !tok || !slot || !pos || !logits || !d_group_off)
+        return fail(DASH_EINVAL, "dash_decode_step_grouped: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (rows < 1 || n_groups < 1 || n_groups > rows) return fail(DASH_EINVAL, "bad n_rows / n_groups");
+    if (group_size < 1 || group_size > kMaxGroupRows) return fail(DASH_ENOTSUP, "group_size must be in [1, %d]", kMaxGroupRows);
+    if (shared_len < 0 || shared_len % kv->g.page_size) return fail(DASH_EINVAL, "shared_len must be a multiple of page_size");
+    int rc = check_ws(m, ws, ws_bytes, rows, kv->max_ctx);
+    if (rc) return rc;
+    if (m->d.dtype != DASH_BF16)  // the fp32 path has no grouped kernel: same results without it
+        return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream);
+    GroupInfo gi{d_group_off, n_groups, group_size, shared_len};
+    return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream, &gi);
+}
+
 int dash_sample(const float* logits, int64_t ld, int32_t rows, int32_t vocab, const int32_t* row_of,
                 const int32_t* uid, const int32_t* step, float temperature, uint64_t seed, int32_t* tok_out,
                 float* lp_out, void* stream) {
@@ -765,6 +796,7 @@ struct RolloutWs {
     int32_t* row_of;
     int32_t* budget;
     int32_t* count;
+    int32_t* group_off;  // [n_prompts + 1]
     size_t bytes;
 };
 
@@ -787,6 +819,7 @@ RolloutWs plan_rollout(const dash_model* m, int n_prompts, int P, int G, int max
     r.row_of = (int32_t*)take((size_t)N * 4);
     r.budget = (int32_t*)take((size_t)N * 4);
     r.count = (int32_t*)take(256);
+    r.group_off = (int32_t*)take((size_t)(n_prompts + 1) * 4);
     r.bytes = off;
     return r;
 }
@@ -874,6 +907,22 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     if ((rc = advance(N))) return rc;
     if ((rc = dash_kv_release(kv, done_at[0].data(), (int)done_at[0].size()))) return rc;
 
+    // prefix-shared groups: the G samples of a prompt share its full prompt pages
+    const int shared_len = (P / kv->g.page_size) * kv->g.page_size;
+    const bool grouped = d.dtype == DASH_BF16 && G <= kMaxGroupRows && G > 1 && shared_len > 0;
+    std::vector<int32_t> goff;
+    GroupInfo gi{rw.group_off, n_prompts, G, shared_len};
+    auto upload_groups = [&](int t) -> int {  // live rows at step t, in sample order, grouped by prompt
+        goff.assign(1, 0);
+        for (int p = 0; p < n_prompts; ++p) {
+            int c = 0;
+            for (int j = 0; j < G; ++j) c += budget[p * G + j] > t;
+            if (c) goff.push_back(goff.back() + c);
+        }
+        gi.n_groups = (int)goff.size() - 1;
+        return kv_upload(kv, rw.group_off, goff.data(), goff.size() * 4, st);
+    };
+    if (grouped && (rc = upload_groups(1))) return rc;
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
     const bool graphs = use_graph && !ragged && st != nullptr;
@@ -896,7 +945,7 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
             if (!exec) {
                 DASH_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
                 g_prof.capturing = true;
-                int rc2 = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st);
+                int rc2 = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st, grouped ? &gi : nullptr);
                 if (!rc2) {
                     hipError_t e = launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
                                                  d_out_tokens, d_out_lp, T, st);
@@ -919,7 +968,8 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
             DASH_HIP(hipGraphLaunch(exec, st));
             continue;
         }
-        if ((rc = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st))) return rc;
+        if (grouped && ragged && t > 1 && (rc = upload_groups(t))) return rc;
+        if ((rc = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st, grouped ? &gi : nullptr))) return rc;
         {
             ProfScope ps(DASH_K_SAMPLE, st);
             DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,

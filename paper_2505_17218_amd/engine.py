@@ -127,6 +127,21 @@ def decode_step(model: Model, kv: KVCache, tokens: torch.Tensor, slots: torch.Te
     return logits
 
 
+def decode_step_grouped(model: Model, kv: KVCache, tokens: torch.Tensor, slots: torch.Tensor, pos: torch.Tensor,
+                        group_off: torch.Tensor, group_size: int, shared_len: int, ws: torch.Tensor | None = None,
+                        logits: torch.Tensor | None = None):
+    """dash_decode_step_grouped: rows [group_off[i], group_off[i+1]) share their first shared_len positions."""
+    n = tokens.numel()
+    if logits is None:
+        logits = torch.empty(n, model.shape.vocab, dtype=torch.float32, device=model.device)
+    if ws is None:
+        ws = model.workspace(n, kv.max_ctx)
+    L.dash_decode_step_grouped(model.handle, kv.handle, tokens.data_ptr(), slots.data_ptr(), pos.data_ptr(), n,
+                               group_off.data_ptr(), group_off.numel() - 1, group_size, shared_len,
+                               logits.data_ptr(), aligned(ws), ws.numel() - 256, stream_handle())
+    return logits
+
+
 def sample(logits: torch.Tensor, seq_uid: torch.Tensor, step: torch.Tensor, temperature: float, seed: int,
            row_of: torch.Tensor | None = None, n_rows: int | None = None, with_logprob: bool = True):
     """dash_sample: returns (int32 tokens [n_rows], float32 logprobs [n_rows] or None)."""
