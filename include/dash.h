@@ -156,15 +156,21 @@ size_t dash_kv_table_bytes(int32_t max_seqs, int32_t max_ctx, int32_t page_size)
  * dash_kv_page_bytes pages, 256-byte aligned) and page-table buffer
  * (dash_kv_table_bytes).  Enqueues a clear of the page table on `stream`.
  * max_ctx bounds every slot's length (prompt + generated tokens).
+ * Decode attention cuts a slot's context into splits whose length is fixed here
+ * from max_seqs, the kv heads and max_ctx (long splits for large capacities,
+ * short ones so that small batches still fill the GPU); a sequence's results in
+ * one cache therefore never depend on which other rows share its batch.
  */
 int dash_kv_create(const dash_model* model, void* d_pool, size_t pool_bytes, int32_t page_size,
                    int32_t max_seqs, int32_t max_ctx, void* d_page_table, void* stream,
                    dash_kv** out);
 void dash_kv_destroy(dash_kv* kv);
 
-/* Pages currently free in the pool, and the current length of one slot. */
+/* Pages currently free in the pool, the current length of one slot, and the
+ * decode-attention split length (keys) chosen at creation. */
 int dash_kv_free_pages(const dash_kv* kv, int32_t* out);
 int dash_kv_slot_len(const dash_kv* kv, int32_t slot, int32_t* out);
+int dash_kv_split_keys(const dash_kv* kv, int32_t* out);
 
 /*
  * Grow the listed slots so that positions [0, new_len) are backed by pages
@@ -304,7 +310,9 @@ int dash_live_compact(const int32_t* d_tok, const int32_t* d_slot, const int32_t
  * The kv handle must have max_seqs >= N, max_ctx >= prompt_len + gen_len and
  * be empty.  d_ws: dash_rollout_workspace_bytes(model, n_prompts, prompt_len, group, kv max_ctx).
  * use_graph != 0 captures the fixed-batch decode step (decode + sample +
- * advance) once as a HIP graph and replays it.
+ * advance) once as a HIP graph and replays it (ragged rollouts, whose batch
+ * shrinks, run eagerly).  Kernel-class timing (dash_profile_enable) also works
+ * under graphs: the timed launches become event-record nodes of the graph.
  */
 size_t dash_rollout_workspace_bytes(const dash_model* model, int32_t n_prompts, int32_t prompt_len,
                                     int32_t group, int32_t max_ctx);
@@ -337,14 +345,18 @@ enum {
 /*
  * While a class's bit is set in `class_mask`, the library brackets each launch
  * of that class with a pair of HIP events on the launch stream and accumulates
- * the elapsed time (GPU clock).  Launches recorded into a HIP graph are not
- * timed.  0 turns timing off.  Not thread-safe.
+ * the elapsed time (GPU clock).  Under stream capture the two records become
+ * event-record nodes of the graph, so each replay times its launches (the
+ * rollout driver reads a replay's times back before replaying that graph
+ * again).  0 turns timing off.  Not thread-safe.
  */
 int dash_profile_enable(uint32_t class_mask);
 
 /* Wait for the pending event pairs, then report per class the summed time in
  * milliseconds (ms_out[DASH_K_COUNT]) and the number of timed launches
- * (launches_out[DASH_K_COUNT]); reset != 0 clears the sums afterwards. */
+ * (launches_out[DASH_K_COUNT]); reset != 0 clears the sums afterwards.
+ * DASH_EDEVICE (outputs still filled) if an event record or read-back failed
+ * since the last call; those launches are missing from the sums. */
 int dash_profile_read(double* ms_out, int64_t* launches_out, int32_t reset);
 
 #ifdef __cplusplus

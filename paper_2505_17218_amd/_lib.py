@@ -51,6 +51,7 @@ _SIGS = {
     "dash_kv_destroy": (None, [_P]),
     "dash_kv_free_pages": (C.c_int, [_P, _I32P]),
     "dash_kv_slot_len": (C.c_int, [_P, C.c_int32, _I32P]),
+    "dash_kv_split_keys": (C.c_int, [_P, _I32P]),
     "dash_kv_reserve": (C.c_int, [_P, _I32P, C.c_int32, C.c_int32, _P]),
     "dash_kv_release": (C.c_int, [_P, _I32P, C.c_int32]),
     "dash_kv_device_status": (C.c_int, [_P, C.POINTER(C.c_uint32), _P]),
@@ -166,6 +167,12 @@ def dash_kv_free_pages(kv: int) -> int:
 def dash_kv_slot_len(kv: int, slot: int) -> int:
     out = C.c_int32()
     _call("dash_kv_slot_len", kv, slot, C.byref(out))
+    return out.value
+
+
+def dash_kv_split_keys(kv: int) -> int:
+    out = C.c_int32()
+    _call("dash_kv_split_keys", kv, C.byref(out))
     return out.value
 
 

@@ -173,13 +173,17 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
     constexpr int ND = HD / 16;
     const int lane = threadIdx.x;
     const int n_kv = g.n_kv;
-    const int row = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv, split = blockIdx.y;
+    // work items (row, kv head) fastest, split slowest, dealt to XCDs in contiguous
+    // runs: the rows of one prompt group read their shared prompt pages through one L2
+    const int wi = xcd_remap(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    const int rk = wi % gridDim.x, split = wi / gridDim.x;
+    const int row = rk / n_kv, kvh = rk % n_kv;
     const int rep = n_heads / n_kv;
     const int head = lane & 15, grp = lane >> 4;
     const int ctx = pos[row] + 1;
     const int sl = slot[row];
     const int nblk = (ctx + 31) >> 5;
-    constexpr int per = kAttnSplitKeys / 32;  // key blocks per split
+    const int per = g.split_keys >> 5;  // key blocks per split
     const int nsplit = min((nblk + per - 1) / per, max_splits);  // rows past max_ctx are not valid input
     if (split >= nsplit) return;
     const int b_begin = split * per;
@@ -268,7 +272,7 @@ decode_attn_group_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict
     // the workgroup walks the blocks of its longest row; shorter rows mask the rest
     int ctx_max = 0;
     for (int i = r0; i < r1; ++i) ctx_max = max(ctx_max, pos[i] + 1);
-    constexpr int per = kAttnSplitKeys / 32;
+    const int per = g.split_keys >> 5;
     const int nblk_wg = (ctx_max + 31) >> 5;
     const int nsplit_wg = min((nblk_wg + per - 1) / per, max_splits);
     if (split >= nsplit_wg) return;  // uniform over the workgroup
@@ -446,10 +450,10 @@ __global__ void __launch_bounds__(64) prefill_attn_bf16_k(const bf16_t* __restri
 // o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
 template <typename T>
 __global__ void combine_k(const float* __restrict__ part, const int32_t* __restrict__ pos, int rows, int n_heads,
-                          int max_splits, int hd, T* __restrict__ o) {
+                          int max_splits, int split_keys, int hd, T* __restrict__ o) {
     const int rh = blockIdx.x;  // row * n_heads + head
     const int row = rh / n_heads;
-    const int ns = min((pos[row] + kAttnSplitKeys) / kAttnSplitKeys, max_splits);  // ceil((pos + 1) / split keys)
+    const int ns = min((pos[row] + split_keys) / split_keys, max_splits);  // ceil((pos + 1) / split keys)
     if (ns <= 1) return;  // written directly by the attention kernel
     const float* ml = part + (size_t)rows * n_heads * max_splits * hd + (size_t)rh * max_splits * 2;
     float M = -INFINITY;
@@ -527,8 +531,15 @@ __global__ void __launch_bounds__(64) attn_generic_k(const T* __restrict__ q, co
 
 }  // namespace
 
+int attention_split_keys(int max_seqs, int n_kv, int max_ctx) {
+    const auto waves = [&](long s) { return (long)max_seqs * n_kv * ((max_ctx + s - 1) / s); };
+    int s = kAttnMinSplitKeys;
+    while (s < max_ctx && s < (1 << 20) && waves(2L * s) >= kAttnTargetWaves) s *= 2;
+    return s;
+}
+
 size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx) {
-    const int ms = (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys;
+    const int ms = (max_ctx + kAttnMinSplitKeys - 1) / kAttnMinSplitKeys;
     if (ms <= 1) return 0;
     return (size_t)rows * n_heads * ms * (head_dim + 2);
 }
@@ -539,7 +550,7 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
     if (rows <= 0) return hipSuccess;
     const float scale = 1.0f / sqrtf((float)g.head_dim);
     if (dtype == 1) {
-        const int ms = std::max(1, (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys);
+        const int ms = std::max(1, (max_ctx + g.split_keys - 1) / g.split_keys);
         dim3 grid(rows * g.n_kv, ms);
         const float sl2 = scale * kLog2e;
         if (g.head_dim == 128)
@@ -566,7 +577,7 @@ hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, co
     if (rows <= 0 || n_groups <= 0) return hipSuccess;
     if (group_size < 1 || group_size > kMaxGroupWaves) return hipErrorInvalidValue;
     const float sl2 = kLog2e / sqrtf((float)g.head_dim);
-    const int ms = std::max(1, (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys);
+    const int ms = std::max(1, (max_ctx + g.split_keys - 1) / g.split_keys);
     dim3 grid(n_groups * g.n_kv, ms);
     const int nw = group_size <= 4 ? 4 : (group_size <= 8 ? 8 : 16);
 #define DASH_GROUP_LAUNCH(HDV, NWV)                                                                              \
@@ -589,10 +600,11 @@ hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, co
 }
 
 hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
-                                    int max_ctx, const float* ws_part, void* o, hipStream_t st) {
-    const int ms = (max_ctx + kAttnSplitKeys - 1) / kAttnSplitKeys;
+                                    int max_ctx, int split_keys, const float* ws_part, void* o, hipStream_t st) {
+    const int ms = (max_ctx + split_keys - 1) / split_keys;
     if (dtype != 1 || ms <= 1 || rows <= 0) return hipSuccess;
-    combine_k<bf16_t><<<rows * n_heads, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, head_dim, (bf16_t*)o);
+    combine_k<bf16_t><<<rows * n_heads, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, split_keys, head_dim,
+                                                     (bf16_t*)o);
     return hipGetLastError();
 }
 

@@ -24,6 +24,17 @@ DASH_DEV bf16_t f2bf(float f) {
     return static_cast<bf16_t>(u >> 16);
 }
 
+// Work-item index for block `bid` of `nb`: the GPU deals consecutive block ids
+// round-robin to its 8 XCDs (each with its own L2), so this gives each XCD one
+// contiguous run of work items instead; neighbouring items (the same weight
+// tile, the rows of one prompt group) then share an L2.
+constexpr int kXcds = 8;
+DASH_DEV int xcd_remap(int bid, int nb) {
+    const int x = bid % kXcds, j = bid / kXcds;
+    const int q = nb / kXcds, r = nb % kXcds;
+    return x * q + (x < r ? x : r) + j;
+}
+
 // Element access for the two storage types (float or bfloat16 bits).
 template <typename T> DASH_DEV float ld_elem(const T* p);
 template <> DASH_DEV float ld_elem<float>(const float* p) { return *p; }
@@ -71,6 +82,7 @@ struct KVGeom {
     int n_layers, n_pages, n_kv, head_dim, page_size;
     int max_pages;  // page-table row length (pages per slot)
     int max_seqs;   // page-table rows (slots)
+    int split_keys; // decode attention context split (multiple of 32, fixed per cache)
 };
 
 // Page backing position `pos` of `slot`, or -1 if the slot, position or table entry is out of range.

@@ -29,20 +29,11 @@ namespace {
 
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
-constexpr int kXcds = 8;
 // Fourth dword of a raw buffer resource on gfx9-family GPUs (stride 0, 32-bit data
 // format): loads past num_records return zeros.
 constexpr int kBufferDword3 = 0x00020000;
 
 DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
-
-// Block id -> work index so that each XCD (block ids congruent mod 8) gets one
-// contiguous run of work items.
-DASH_DEV int xcd_remap(int bid, int nb) {
-    const int x = bid % kXcds, j = bid / kXcds;
-    const int q = nb / kXcds, r = nb % kXcds;
-    return x * q + (x < r ? x : r) + j;
-}
 
 // On gfx950 the 32x32x16 bf16 MFMA sustains about twice the rate of 16x16x32
 // (measured: ~2.1 vs ~1.24 PFLOP/s with register-only operands), so the main

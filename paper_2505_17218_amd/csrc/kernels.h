@@ -50,14 +50,21 @@ int gemm_pick_splits(int dtype, int epi, int N, int K);
 
 // ---- attention (attention.hip) ----
 // Decode attention over the paged cache for rows with 1 query each.  bf16: MFMA
-// kernel; a row's context is cut into splits of kAttnSplitKeys keys (depending on
-// its own length only, so results are batch-invariant) merged by a second kernel;
-// partials live in ws_part (attention_partial_floats).  fp32: generic kernel.
-// q [rows][Hq][hd]; o [rows][Hq*hd].
-constexpr int kAttnSplitKeys = 512;
+// kernel; a row's context is cut into splits of g.split_keys keys (depending on
+// its own length and the cache only, so results are batch-invariant) merged by a
+// second kernel; partials live in ws_part (attention_partial_floats).  fp32:
+// generic kernel.  q [rows][Hq][hd]; o [rows][Hq*hd].
+constexpr int kAttnMinSplitKeys = 256;
+constexpr int kAttnTargetWaves = 2048;  // 2 waves per SIMD over 256 CUs
+// Split length for a cache: the largest power of two >= kAttnMinSplitKeys whose
+// split count still gives max_seqs * n_kv * splits >= kAttnTargetWaves at max_ctx
+// (and no longer than max_ctx needs).  Long splits mean fewer partials to write and
+// merge; short ones give small batches enough waves.
+int attention_split_keys(int max_seqs, int n_kv, int max_ctx);
 hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
                                    const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                    int n_heads, void* o, int rows, int max_ctx, float* ws_part, hipStream_t st);
+// Partial-result floats for any cache of this max_ctx (sized for the shortest split).
 size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx);
 // Decode attention for batches made of groups of rows that share a prefix: rows
 // [group_off[i], group_off[i+1]) (at most group_size <= 16 of them) share their first
@@ -70,7 +77,7 @@ hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, co
                                            hipStream_t st);
 // Second pass of decode attention: merge the splits of rows longer than one split (bf16 only).
 hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
-                                    int max_ctx, const float* ws_part, void* o, hipStream_t st);
+                                    int max_ctx, int split_keys, const float* ws_part, void* o, hipStream_t st);
 // Causal attention of prefill rows: rows are whole prompts of prompt_len positions, row
 // r = prompt * prompt_len + position, all rows of a prompt in slot[prompt * prompt_len].
 // bf16: MFMA kernel; fp32: generic kernel (row r attends to 0..pos[r] of slot[r]).

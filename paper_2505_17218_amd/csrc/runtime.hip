@@ -50,6 +50,10 @@ constexpr int kMaxGroupRows = 8;  // rows per prefix-shared group the grouped ke
 // ------------------------------------------------------------- profiler ----
 // Event pairs around launches, by kernel class; a ring of pairs is harvested
 // lazily (a pair is read back only when its slot is reused or on read-out).
+// Under stream capture the pairs become event-record nodes of the graph (a set
+// per captured graph, re-armed by every replay and harvested before the next).
+
+struct GraphProf;
 
 struct Profiler {
     struct Pair {
@@ -61,27 +65,104 @@ struct Profiler {
     bool capturing = false;
     std::vector<Pair> ring;
     size_t next = 0;
+    GraphProf* capture_set = nullptr;  // hands out the pairs recorded while capturing
     double ms[DASH_K_COUNT] = {};
     int64_t n[DASH_K_COUNT] = {};
+    std::string err;  // first timing failure since the last read-out
 };
 Profiler g_prof;
 
+void prof_error(const char* what, hipError_t e, int cls = -1, int idx = -1) {
+    if (g_prof.err.empty()) {
+        char buf[256];
+        snprintf(buf, sizeof buf, "%s (class %d, pair %d): %s", what, cls, idx, hipGetErrorString(e));
+        g_prof.err = buf;
+    }
+    (void)hipGetLastError();
+}
+
 void prof_harvest(Profiler::Pair& p) {
     if (!p.live) return;
-    float ms = 0.f;
-    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
-        g_prof.ms[p.cls] += ms;
-        g_prof.n[p.cls] += 1;
-    }
     p.live = false;
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(p.b);
+    if (e != hipSuccess) return prof_error("hipEventSynchronize", e);
+    if ((e = hipEventElapsedTime(&ms, p.a, p.b)) != hipSuccess) return prof_error("hipEventElapsedTime", e);
+    g_prof.ms[p.cls] += ms;
+    g_prof.n[p.cls] += 1;
 }
+
+// Append an event-record node to the capture in progress on `st` (after the
+// nodes captured so far; later captured work depends on it).  Explicit nodes
+// rather than hipEventRecordWithFlags(hipEventRecordExternal), which some HIP
+// runtime builds reject during capture.
+hipError_t capture_event_record(hipStream_t st, hipEvent_t ev) {
+    hipStreamCaptureStatus cs;
+    unsigned long long id;
+    hipGraph_t g;
+    const hipGraphNode_t* deps;
+    size_t nd;
+    hipError_t e = hipStreamGetCaptureInfo_v2(st, &cs, &id, &g, &deps, &nd);
+    if (e != hipSuccess) return e;
+    if (cs != hipStreamCaptureStatusActive) return hipErrorIllegalState;
+    hipGraphNode_t node;
+    if ((e = hipGraphAddEventRecordNode(&node, g, deps, nd, ev)) != hipSuccess) return e;
+    return hipStreamUpdateCaptureDependencies(st, &node, 1, hipStreamSetCaptureDependencies);
+}
+
+// Timed pairs of one captured graph.  Events cannot be created during capture,
+// so the pairs are created beforehand (reserve) and handed out by ProfScope.
+struct GraphProf {
+    std::vector<Profiler::Pair> pairs;
+    size_t used = 0;
+    bool reserve(size_t n) {
+        while (pairs.size() < n) {
+            Profiler::Pair p;
+            if (hipEventCreate(&p.a) != hipSuccess) return false;
+            if (hipEventCreate(&p.b) != hipSuccess) {
+                (void)hipEventDestroy(p.a);
+                return false;
+            }
+            pairs.push_back(p);
+        }
+        return true;
+    }
+    void armed() {  // after a replay was launched
+        for (size_t i = 0; i < used; ++i) pairs[i].live = true;
+    }
+    void harvest() {
+        for (auto& p : pairs) prof_harvest(p);
+    }
+    ~GraphProf() {
+        harvest();
+        for (auto& p : pairs) {
+            (void)hipEventDestroy(p.a);
+            (void)hipEventDestroy(p.b);
+        }
+    }
+};
 
 // Times the launches made during its lifetime if class `cls` is enabled (cls < 0: never).
 struct ProfScope {
     int slot = -1;
     hipStream_t st;
+    Profiler::Pair* gp = nullptr;  // capture mode: a pair of the graph's set
     ProfScope(int cls, hipStream_t s) : st(s) {
-        if (cls < 0 || !(g_prof.mask & (1u << cls)) || g_prof.capturing || g_prof.ring.empty()) return;
+        if (cls < 0 || !(g_prof.mask & (1u << cls))) return;
+        if (g_prof.capturing) {
+            GraphProf* set = g_prof.capture_set;
+            if (!set || set->used >= set->pairs.size()) return;
+            Profiler::Pair& p = set->pairs[set->used];
+            const hipError_t e = capture_event_record(st, p.a);
+            if (e != hipSuccess) {
+                prof_error("start record under capture", e, cls, (int)set->used);
+                return;
+            }
+            p.cls = cls;
+            gp = &p;
+            return;
+        }
+        if (g_prof.ring.empty()) return;
         Profiler::Pair& p = g_prof.ring[g_prof.next];
         prof_harvest(p);
         if (hipEventRecord(p.a, st) != hipSuccess) return;
@@ -90,6 +171,12 @@ struct ProfScope {
         g_prof.next = (g_prof.next + 1) % g_prof.ring.size();
     }
     ~ProfScope() {
+        if (gp) {
+            const hipError_t e = capture_event_record(st, gp->b);
+            if (e == hipSuccess) g_prof.capture_set->used++;
+            else prof_error("end record under capture", e, gp->cls, (int)g_prof.capture_set->used);
+            return;
+        }
         if (slot < 0) return;
         Profiler::Pair& p = g_prof.ring[slot];
         p.live = hipEventRecord(p.b, st) == hipSuccess;
@@ -337,7 +424,8 @@ int dash_kv_create(const dash_model* m, void* pool, size_t pool_bytes, int32_t p
     kv->pool = pool;
     kv->max_ctx = max_ctx;
     const int max_pages = (max_ctx + ps - 1) / ps;
-    kv->g = KVGeom{m->d.n_layers, (int)pages, m->d.n_kv_heads, m->d.head_dim, ps, max_pages, max_seqs};
+    kv->g = KVGeom{m->d.n_layers, (int)pages, m->d.n_kv_heads, m->d.head_dim, ps, max_pages, max_seqs,
+                   attention_split_keys(max_seqs, m->d.n_kv_heads, max_ctx)};
     const size_t ent = table_entries(max_seqs, max_ctx, ps);
     kv->d_table = (int32_t*)d_table;
     kv->d_status = (uint32_t*)((char*)d_table + align_up(ent * 4, 256));
@@ -396,6 +484,12 @@ int dash_kv_slot_len(const dash_kv* kv, int32_t slot, int32_t* out) {
     if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
     if (slot < 0 || slot >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", slot);
     *out = kv->len[slot];
+    return DASH_OK;
+}
+
+int dash_kv_split_keys(const dash_kv* kv, int32_t* out) {
+    if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
+    *out = kv->g.split_keys;
     return DASH_OK;
 }
 
@@ -485,6 +579,11 @@ int dash_profile_read(double* ms_out, int64_t* launches_out, int32_t reset) {
             g_prof.n[i] = 0;
         }
     }
+    if (!g_prof.err.empty()) {
+        const std::string e = g_prof.err;
+        g_prof.err.clear();
+        return fail(DASH_EDEVICE, "kernel timing failed: %s", e.c_str());
+    }
     return DASH_OK;
 }
 
@@ -562,7 +661,8 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
                                                      w.o, rows, kv->max_ctx, w.attn_part, st));
             }
             ProfScope ps(DASH_K_ATTN_COMBINE, st);
-            DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, w.attn_part, w.o, st));
+            DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, kv->g.split_keys,
+                                              w.attn_part, w.o, st));
         }
         {
             ProfScope ps(cls(DASH_K_GEMM_O), st);
@@ -796,7 +896,6 @@ struct RolloutWs {
     int32_t* row_of;
     int32_t* budget;
     int32_t* count;
-    int32_t* group_off;  // [n_prompts + 1]
     size_t bytes;
 };
 
@@ -819,7 +918,6 @@ RolloutWs plan_rollout(const dash_model* m, int n_prompts, int P, int G, int max
     r.row_of = (int32_t*)take((size_t)N * 4);
     r.budget = (int32_t*)take((size_t)N * 4);
     r.count = (int32_t*)take(256);
-    r.group_off = (int32_t*)take((size_t)(n_prompts + 1) * 4);
     r.bytes = off;
     return r;
 }
@@ -907,25 +1005,56 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     if ((rc = advance(N))) return rc;
     if ((rc = dash_kv_release(kv, done_at[0].data(), (int)done_at[0].size()))) return rc;
 
-    // prefix-shared groups: the G samples of a prompt share its full prompt pages
-    const int shared_len = (P / kv->g.page_size) * kv->g.page_size;
-    const bool grouped = d.dtype == DASH_BF16 && G <= kMaxGroupRows && G > 1 && shared_len > 0;
-    std::vector<int32_t> goff;
-    GroupInfo gi{rw.group_off, n_prompts, G, shared_len};
-    auto upload_groups = [&](int t) -> int {  // live rows at step t, in sample order, grouped by prompt
-        goff.assign(1, 0);
-        for (int p = 0; p < n_prompts; ++p) {
-            int c = 0;
-            for (int j = 0; j < G; ++j) c += budget[p * G + j] > t;
-            if (c) goff.push_back(goff.back() + c);
-        }
-        gi.n_groups = (int)goff.size() - 1;
-        return kv_upload(kv, rw.group_off, goff.data(), goff.size() * 4, st);
-    };
-    if (grouped && (rc = upload_groups(1))) return rc;
-    hipGraph_t graph = nullptr;
-    hipGraphExec_t exec = nullptr;
+    // Decode steps.  With graphs, one step (decode + sample + advance) is captured
+    // once and replayed; when kernel classes are being timed, two copies are
+    // captured, each with its own events, and replayed alternately so that one
+    // copy's timings are read back while the other runs.
     const bool graphs = use_graph && !ragged && st != nullptr;
+    const int n_exec = graphs && g_prof.mask ? 2 : 1;
+    hipGraphExec_t exec[2] = {nullptr, nullptr};
+    GraphProf gprof[2];
+    int64_t replays = 0;
+    auto destroy_graphs = [&]() {
+        for (int i = 0; i < 2; ++i)
+            if (exec[i]) {
+                gprof[i].harvest();
+                (void)hipGraphExecDestroy(exec[i]);
+                exec[i] = nullptr;
+            }
+    };
+    auto one_step = [&](int B) -> int {
+        int rc2 = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st);
+        if (rc2) return rc2;
+        {
+            ProfScope ps(DASH_K_SAMPLE, st);
+            DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
+                                   d_out_tokens, d_out_lp, T, st));
+        }
+        ProfScope ps(DASH_K_OTHER, st);
+        return advance(B);
+    };
+    auto capture = [&](int i, int B) -> int {
+        // timed launches per step: at most 12 per layer plus a few outside the layers
+        if (g_prof.mask && !gprof[i].reserve(12 * (size_t)d.n_layers + 16))
+            return fail(DASH_EDEVICE, "hipEventCreate failed");
+        DASH_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+        g_prof.capturing = true;
+        g_prof.capture_set = &gprof[i];
+        const int rc2 = one_step(B);
+        g_prof.capturing = false;
+        g_prof.capture_set = nullptr;
+        hipGraph_t graph = nullptr;
+        hipError_t e = hipStreamEndCapture(st, &graph);
+        if (rc2) {
+            if (graph) (void)hipGraphDestroy(graph);
+            return rc2;
+        }
+        if (e != hipSuccess) return fail(DASH_EDEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
+        e = hipGraphInstantiate(&exec[i], graph, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(graph);
+        if (e != hipSuccess) return fail(DASH_EDEVICE, "hipGraphInstantiate: %s", hipGetErrorString(e));
+        return DASH_OK;
+    };
     std::vector<int32_t> live_slots;
     for (int t = 1; t < T; ++t) {
         const int B = ragged ? live_after[t] : N;
@@ -939,50 +1068,31 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
             // one page ahead, capped at the last position the sample will feed (P + budget - 2)
             const int ahead = (need_len + kv->g.page_size - 1) / kv->g.page_size * kv->g.page_size;
             for (int s : live_slots) kv_grow(kv, s, std::min(P + budget[s] - 1, ahead));
-            if ((rc = kv_push_rows(kv, live_slots.front(), live_slots.back(), st))) return rc;
+            if ((rc = kv_push_rows(kv, live_slots.front(), live_slots.back(), st))) {
+                destroy_graphs();
+                return rc;
+            }
         }
         if (graphs) {
-            if (!exec) {
-                DASH_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
-                g_prof.capturing = true;
-                int rc2 = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st, grouped ? &gi : nullptr);
-                if (!rc2) {
-                    hipError_t e = launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
-                                                 d_out_tokens, d_out_lp, T, st);
-                    if (e == hipSuccess) e = launch_rows_advance(S[2], S[3], B, st);
-                    if (e != hipSuccess) rc2 = fail(DASH_EDEVICE, "launch during capture: %s", hipGetErrorString(e));
-                }
-                g_prof.capturing = false;
-                hipError_t e = hipStreamEndCapture(st, &graph);
-                if (rc2) {
-                    if (graph) (void)hipGraphDestroy(graph);
-                    return rc2;
-                }
-                if (e != hipSuccess) return fail(DASH_EDEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
-                e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-                if (e != hipSuccess) {
-                    (void)hipGraphDestroy(graph);
-                    return fail(DASH_EDEVICE, "hipGraphInstantiate: %s", hipGetErrorString(e));
-                }
+            const int i = (int)(replays % n_exec);
+            if (!exec[i] && (rc = capture(i, B))) {
+                destroy_graphs();
+                return rc;
             }
-            DASH_HIP(hipGraphLaunch(exec, st));
+            gprof[i].harvest();  // the timings of this copy's previous replay
+            const hipError_t e = hipGraphLaunch(exec[i], st);
+            if (e != hipSuccess) {
+                destroy_graphs();
+                return fail(DASH_EDEVICE, "hipGraphLaunch: %s", hipGetErrorString(e));
+            }
+            gprof[i].armed();
+            ++replays;
             continue;
         }
-        if (grouped && ragged && t > 1 && (rc = upload_groups(t))) return rc;
-        if ((rc = decode_step_impl(m, kv, S[0], S[1], S[2], B, rw.logits, ws, st, grouped ? &gi : nullptr))) return rc;
-        {
-            ProfScope ps(DASH_K_SAMPLE, st);
-            DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
-                                   d_out_tokens, d_out_lp, T, st));
-        }
-        {
-            ProfScope ps(DASH_K_OTHER, st);
-            if ((rc = advance(B))) return rc;
-        }
+        if ((rc = one_step(B))) return rc;
         if (ragged && (rc = dash_kv_release(kv, done_at[t].data(), (int)done_at[t].size()))) return rc;
     }
-    if (exec) (void)hipGraphExecDestroy(exec);
-    if (graph) (void)hipGraphDestroy(graph);
+    destroy_graphs();
     // release whatever is still held (fixed-length rollouts end with every slot live)
     std::vector<int32_t> held;
     for (int i = 0; i < N; ++i)

@@ -84,6 +84,10 @@ class KVCache:
     def free_pages(self) -> int:
         return L.dash_kv_free_pages(self.handle)
 
+    @property
+    def split_keys(self) -> int:
+        return L.dash_kv_split_keys(self.handle)
+
     def close(self):
         if getattr(self, "handle", None):
             torch.cuda.synchronize()

@@ -76,6 +76,23 @@ def test_bf16_stepwise_matches_oracle(shape, n_prompts, G, P, T):
     print(f"{shape.name} P={P} T={T}: max |dlogits| = {worst:.3g}")
 
 
+@pytest.mark.parametrize("max_seqs,split", [(4, 256), (1024, 1024)])
+def test_bf16_split_length_follows_capacity(max_seqs, split):
+    """The decode-attention split length is fixed per cache from its capacity: a small
+    cache cuts a 600-key context into 256-key splits merged by the combine kernel, a
+    large one reads it as a single 1024-key split.  Both match the oracle."""
+    shape = BF16_A
+    w = synth.make_weights(shape, 1)
+    wl = synth.Workload("t", shape, 2, 2, 600, 6)
+    prompts = synth.make_prompts(wl, 1)
+    model = engine.Model(shape, w)
+    kv = engine.KVCache(model, 32, max_seqs, 606, 4 * 19 + 8)  # pages for the 4 rows used
+    assert kv.split_keys == split
+    run = run_stepwise(model, kv, prompts, 2, 6, 1.0, 77)
+    worst = _check_run(shape, w, prompts, 2, 6, run, 1.0, 77, TOL[shape.dtype])
+    print(f"split {split}: max |dlogits| = {worst:.3g}")
+
+
 def test_bf16_large_batch_gemm_tiles():
     """160 decode rows (M > 128 with a tail) through the MFMA GEMMs; checked on sampled rows."""
     shape = BF16_A
@@ -155,6 +172,34 @@ def test_rollout_driver_matches_stepwise_tiny():
         np.testing.assert_array_equal(toks.cpu().numpy(), step.tokens)
         np.testing.assert_array_equal(lps.cpu().numpy(), step.logprobs)
     assert kv.free_pages == kv.pool.numel() // L.dash_kv_page_bytes(model.handle, 16)
+
+
+def test_rollout_graph_profiling_times_every_launch():
+    """Kernel-class timing under graph replay: each decode step's attention launches
+    are event-record nodes of the graph; every replay is counted once, with the same
+    tokens as an untimed run."""
+    shape = BF16_A
+    w = synth.make_weights(shape, 6)
+    n_prompts, G, P, T = 2, 4, 70, 9
+    prompts = synth.make_prompts(synth.Workload("t", shape, n_prompts, G, P, T), 6)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, n_prompts * G, P + T)
+    ro = engine.Rollout(model, kv, n_prompts, P, G, T)
+    plain, _ = ro.run(dev_i32(prompts), 1.0, 3, use_graph=True)
+    plain = plain.cpu().numpy().copy()
+    L.dash_profile_read(reset=True)
+    L.dash_profile_enable((1 << L.K["attn"]) | (1 << L.K["sample"]))
+    try:
+        timed, _ = ro.run(dev_i32(prompts), 1.0, 3, use_graph=True)
+        torch.cuda.synchronize()
+        prof = L.dash_profile_read(reset=True)
+    finally:
+        L.dash_profile_enable(0)
+    np.testing.assert_array_equal(timed.cpu().numpy(), plain)
+    ms, n = prof["attn"]
+    assert n == shape.n_layers * (T - 1) and ms > 0
+    assert prof["sample"][1] == T - 1  # the first token is sampled outside the decode loop, untimed
+    assert prof["gemm_qkv"][1] == 0
 
 
 @pytest.mark.parametrize("shape", [BF16_A, BF16_B])
