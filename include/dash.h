@@ -352,6 +352,12 @@ enum {
  */
 int dash_profile_enable(uint32_t class_mask);
 
+/* Limit the timing of per-layer classes (norm, rope, attention, the layer
+ * GEMMs) to the launches of decoder layer `layer`; -1 (the default) times every
+ * layer.  Every layer runs the same kernels on the same shapes, so one layer's
+ * launches give the average launch time with a fraction of the event records. */
+int dash_profile_layer(int32_t layer);
+
 /* Wait for the pending event pairs, then report per class the summed time in
  * milliseconds (ms_out[DASH_K_COUNT]) and the number of timed launches
  * (launches_out[DASH_K_COUNT]); reset != 0 clears the sums afterwards.

@@ -68,6 +68,7 @@ _SIGS = {
     "dash_rollout": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _I32P, C.c_float, C.c_uint64,
                                _P, _P, C.c_int32, _P, C.c_size_t, _P]),
     "dash_profile_enable": (C.c_int, [C.c_uint32]),
+    "dash_profile_layer": (C.c_int, [C.c_int32]),
     "dash_profile_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]),
 }
 
@@ -239,6 +240,10 @@ def dash_rollout(model, kv, d_prompts, n_prompts, prompt_len, group, gen_len, bu
 
 def dash_profile_enable(class_mask: int) -> None:
     _call("dash_profile_enable", class_mask)
+
+
+def dash_profile_layer(layer: int) -> None:
+    _call("dash_profile_layer", layer)
 
 
 def dash_profile_read(reset: bool = True) -> dict:

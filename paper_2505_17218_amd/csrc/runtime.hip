@@ -69,6 +69,7 @@ struct Profiler {
     double ms[DASH_K_COUNT] = {};
     int64_t n[DASH_K_COUNT] = {};
     std::string err;  // first timing failure since the last read-out
+    int layer = -1;   // >= 0: per-layer classes are timed in this layer only
 };
 Profiler g_prof;
 
@@ -569,6 +570,12 @@ int dash_profile_enable(uint32_t class_mask) {
     return DASH_OK;
 }
 
+int dash_profile_layer(int32_t layer) {
+    if (layer < -1) return fail(DASH_EINVAL, "layer must be >= -1");
+    g_prof.layer = layer;
+    return DASH_OK;
+}
+
 int dash_profile_read(double* ms_out, int64_t* launches_out, int32_t reset) {
     for (auto& p : g_prof.ring) prof_harvest(p);
     for (int i = 0; i < DASH_K_COUNT; ++i) {
@@ -625,12 +632,17 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
     const int sq = gemm_pick_splits(dt, EPI_STORE_F32, qr, d.d_model);
     const int so = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, hq);
     const int sd = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, d.d_ff);
-    auto cls = [&](int c) { return prefill ? -1 : c; };  // prefill is timed as one class by its caller
+    // prefill is timed as one class by its caller; per-layer classes may be limited to one layer
+    int cur_layer = -1;
+    auto cls = [&](int c) {
+        return prefill || (g_prof.layer >= 0 && cur_layer >= 0 && cur_layer != g_prof.layer) ? -1 : c;
+    };
     {
         ProfScope ps(cls(DASH_K_ROPE), st);
         DASH_HIP(launch_rope_table(pos, w.cs, rows, d.head_dim, d.rope_theta, st));
     }
     for (int l = 0; l < d.n_layers; ++l) {
+        cur_layer = l;
         if (l > 0) {
             ProfScope ps(cls(DASH_K_NORM), st);
             DASH_HIP(launch_add_rmsnorm(dt, w.x, w.delta, sd, (size_t)rows * d.d_model, m->lw(l, 0), w.y, nullptr, rows,
@@ -651,7 +663,7 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
                                               prefill_len, st));
         } else {
             {
-                ProfScope ps(DASH_K_ATTN, st);
+                ProfScope ps(cls(DASH_K_ATTN), st);
                 if (gi)
                     DASH_HIP(launch_decode_attention_grouped(w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads,
                                                              gi->off, gi->n_groups, gi->group_size, gi->shared_len,
@@ -660,7 +672,7 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
                     DASH_HIP(launch_decode_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads,
                                                      w.o, rows, kv->max_ctx, w.attn_part, st));
             }
-            ProfScope ps(DASH_K_ATTN_COMBINE, st);
+            ProfScope ps(cls(DASH_K_ATTN_COMBINE), st);
             DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, kv->g.split_keys,
                                               w.attn_part, w.o, st));
         }

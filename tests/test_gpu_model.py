@@ -200,6 +200,17 @@ def test_rollout_graph_profiling_times_every_launch():
     assert n == shape.n_layers * (T - 1) and ms > 0
     assert prof["sample"][1] == T - 1  # the first token is sampled outside the decode loop, untimed
     assert prof["gemm_qkv"][1] == 0
+    # one layer's launches only
+    L.dash_profile_enable(1 << L.K["attn"])
+    L.dash_profile_layer(1)
+    try:
+        ro.run(dev_i32(prompts), 1.0, 3, use_graph=True)
+        torch.cuda.synchronize()
+        prof = L.dash_profile_read(reset=True)
+    finally:
+        L.dash_profile_enable(0)
+        L.dash_profile_layer(-1)
+    assert prof["attn"][1] == T - 1 and prof["attn"][0] > 0
 
 
 @pytest.mark.parametrize("shape", [BF16_A, BF16_B])
