@@ -266,6 +266,18 @@ int dash_sample(const float* d_logits, int64_t ld, int32_t n_rows, int32_t vocab
                 int32_t* d_tokens_out, float* d_logprob_out, void* stream);
 
 /*
+ * Self-check of the sampler's screening.  dash_sample first scores every entry
+ * with a cheap noise (hardware logarithm) and computes the exact noise only for
+ * entries that can still win; this is exact provided the cheap noise is within
+ * the tolerance of the exact one for every possible u.  This call measures the
+ * largest |cheap - exact| over all 2^23 values u can take, on the current
+ * device, and returns it with the tolerance the sampler assumes (h_max_err <
+ * h_tol means the screening is exact here).  Synchronous; allocates 256 bytes
+ * of device memory for the duration of the call.
+ */
+int dash_sampler_check(double* h_max_err, double* h_tol);
+
+/*
  * GRPO group advantage (Sec. 3.3, Eq. (4)) and gradient filter (Sec. 3.5).
  * d_rewards: float32 [n_groups * group], group k = samples k*group .. k*group+group-1.
  * mean = S(r)/G, d = r - mean, A = d (MEAN_ONLY) or d / (sqrt(S(d*d)/(G - ddof)) + eps)

@@ -61,6 +61,7 @@ _SIGS = {
     "dash_decode_step_grouped": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, C.c_int32, C.c_int32, C.c_int32, _P,
                                            _P, C.c_size_t, _P]),
     "dash_sample": (C.c_int, [_P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P, C.c_float, C.c_uint64, _P, _P, _P]),
+    "dash_sampler_check": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_double)]),
     "dash_group_advantage_filter": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float, _P, _P,
                                               _P, _P]),
     "dash_live_compact": (C.c_int, [_P, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P, _P]),
@@ -236,6 +237,13 @@ def dash_rollout(model, kv, d_prompts, n_prompts, prompt_len, group, gen_len, bu
     b = i32_array(budgets) if budgets is not None else None
     _call("dash_rollout", model, kv, d_prompts, n_prompts, prompt_len, group, gen_len, b, C.c_float(temperature),
           C.c_uint64(seed), d_out_tokens, d_out_logprobs, int(use_graph), d_ws, ws_bytes, stream)
+
+
+def dash_sampler_check() -> tuple[float, float]:
+    """(largest |cheap - exact| Gumbel noise over all inputs, the sampler's screening tolerance)."""
+    err, tol = C.c_double(), C.c_double()
+    _call("dash_sampler_check", C.byref(err), C.byref(tol))
+    return err.value, tol.value
 
 
 def dash_profile_enable(class_mask: int) -> None:

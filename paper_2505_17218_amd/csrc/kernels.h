@@ -86,6 +86,11 @@ hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos
                                     int n_heads, void* o, int rows, int prompt_len, hipStream_t st);
 
 // ---- sampling / advantage (sampler.hip, advantage.hip) ----
+// Screening tolerance of the sampler, and an exhaustive check of it: the largest
+// |cheap noise - exact noise| over all noise values, as float bits, max-reduced
+// into *d_max_err_bits (which must start at 0).
+float sampler_screen_tol();
+hipError_t launch_sampler_screen_check(unsigned* d_max_err_bits, hipStream_t st);
 hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
                          const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
                          int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,

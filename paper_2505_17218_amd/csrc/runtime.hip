@@ -873,6 +873,23 @@ int dash_sample(const float* logits, int64_t ld, int32_t rows, int32_t vocab, co
     return DASH_OK;
 }
 
+int dash_sampler_check(double* h_max_err, double* h_tol) {
+    if (!h_max_err || !h_tol) return fail(DASH_EINVAL, "dash_sampler_check: NULL argument");
+    unsigned* d = nullptr;
+    DASH_HIP(hipMalloc(&d, 256));
+    unsigned bits = 0;
+    hipError_t e = hipMemset(d, 0, 4);
+    if (e == hipSuccess) e = launch_sampler_screen_check(d, nullptr);
+    if (e == hipSuccess) e = hipMemcpy(&bits, d, 4, hipMemcpyDeviceToHost);
+    (void)hipFree(d);
+    if (e != hipSuccess) return fail(DASH_EDEVICE, "sampler check: %s", hipGetErrorString(e));
+    float f;
+    memcpy(&f, &bits, 4);
+    *h_max_err = f;
+    *h_tol = sampler_screen_tol();
+    return DASH_OK;
+}
+
 int dash_group_advantage_filter(const float* r, int32_t n_groups, int32_t group, int32_t mode, float eps, float tau,
                                 float* adv, int32_t* kept, int32_t* count, void* stream) {
     if (!r || !adv || !kept || !count) return fail(DASH_EINVAL, "dash_group_advantage_filter: NULL argument");

@@ -5,9 +5,20 @@
 // stride of 256 groups, so a wave reads 1 KB of logits per step, coalesced.
 // Each thread keeps its best (score, index) and an online (max, sum of exp) for
 // the log-normaliser; waves merge with xor shuffles, then LDS merges the four
-// waves.  Ties in the score go to the smaller vocab index.  The kernel is ALU
-// bound (ten Philox rounds per four entries and two logs per entry), not HBM
-// bound.  Built with -ffp-contract=off: see sampler_math.h.
+// waves.  Ties in the score go to the smaller vocab index.  Built with
+// -ffp-contract=off: see sampler_math.h.
+//
+// Screening.  The exact noise -ln(-ln u) (two correctly rounded divisions) is
+// the expensive part, so every entry is first scored with a cheap noise from the
+// hardware logarithm, whose distance to the exact noise is below kScreenTol for
+// every value u can take (checked exhaustively by dash_sampler_check).  With the
+// fp32 rounding of the sums added, each entry's exact score lies within a margin
+// of its cheap score.  The wave keeps a shared lower bound on the best exact
+// score seen so far (exact scores of evaluated entries, cheap score minus margin
+// of the rest); an entry whose cheap score plus margin falls below it cannot be
+// the argmax and is skipped, every other entry gets its exact score.  The winner
+// is therefore always evaluated exactly: tokens are bit-identical to scoring
+// every entry exactly.
 #include "common.h"
 #include "kernels.h"
 #include "sampler_math.h"
@@ -17,8 +28,25 @@ namespace dash {
 namespace {
 
 constexpr int kThreads = 256;
+// bound on |cheap noise - exact noise|: 8x the exhaustive maximum (1.9e-6) on gfx950
+constexpr float kScreenTol = 1.6e-5f;
 
 DASH_DEV bool better(float s, int i, float bs, int bi) { return s > bs || (s == bs && i < bi); }
+
+// -ln(-ln u) with the hardware logarithm; u = ((x >> 8) | 1) 2^-24 as in gumbel_from_bits
+DASH_DEV float cheap_gumbel(uint32_t x) {
+    const float u = (float)((x >> 8) | 1u) * (1.0f / 16777216.0f);
+    return -__logf(-__logf(u));
+}
+
+// Interval half-width around a cheap score sa that contains the exact score.
+DASH_DEV float screen_margin(float sa) { return kScreenTol + fabsf(sa) * (1.0f / 1048576.0f); }
+
+DASH_DEV float wave_max_f(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
 
 __global__ void __launch_bounds__(kThreads)
 sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ row_of,
@@ -38,34 +66,49 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     float best_s = -INFINITY;
     int best_i = 0x7FFFFFFF;
     float mx = -INFINITY, z = 0.f;
+    float floor_w = -INFINITY;  // wave-shared lower bound on the best exact score seen
     const int n4 = (vocab + 3) >> 2;
-    for (int g = threadIdx.x; g < n4; g += kThreads) {
-        float l[4];
-        if (vec4 && 4 * g + 3 < vocab) {
-            const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
-            l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
-        }
-        const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, k0, k1);
-        const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (!isfinite(l[j])) continue;
-            const float sc = unit_t ? l[j] : div_rn(l[j], temperature);
-            const float s = sc + gumbel_from_bits(xs[j]);
-            if (s > best_s) {  // indices grow within a thread: strict > keeps the smallest on ties
-                best_s = s;
-                best_i = 4 * g + j;
-            }
-            if (sc > mx) {
-                z = z * __expf(mx - sc) + 1.0f;
-                mx = sc;
+    // every lane of the wave runs the same number of iterations (the shared bound needs all lanes)
+    const int lane0 = threadIdx.x & ~63;
+    for (int g0 = lane0; g0 < n4; g0 += kThreads) {
+        const int g = g0 + (threadIdx.x & 63);
+        float floor_t = floor_w;
+        if (g < n4) {
+            float l[4];
+            if (vec4 && 4 * g + 3 < vocab) {
+                const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
+                l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
             } else {
-                z += __expf(sc - mx);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
+            }
+            const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, k0, k1);
+            const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (!isfinite(l[j])) continue;
+                const float sc = unit_t ? l[j] : div_rn(l[j], temperature);
+                const float sa = sc + cheap_gumbel(xs[j]);
+                const float mg = screen_margin(sa);
+                if (sa + mg >= floor_t) {
+                    const float s = sc + gumbel_from_bits(xs[j]);  // exact
+                    if (s > best_s) {  // indices grow within a thread: strict > keeps the smallest on ties
+                        best_s = s;
+                        best_i = 4 * g + j;
+                    }
+                    floor_t = fmaxf(floor_t, s);
+                } else {
+                    floor_t = fmaxf(floor_t, sa - mg);
+                }
+                if (sc > mx) {
+                    z = z * __expf(mx - sc) + 1.0f;
+                    mx = sc;
+                } else {
+                    z += __expf(sc - mx);
+                }
             }
         }
+        floor_w = wave_max_f(floor_t);
     }
     // wave merge
 #pragma unroll
@@ -112,7 +155,24 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     if (traj_lp) traj_lp[(size_t)u_id * traj_ld + st] = lp;
 }
 
+// Largest |cheap noise - exact noise| over every value u can take: (x >> 8) | 1
+// is odd, so x = (2k + 1) << 8 for k < 2^23 covers them all.
+__global__ void screen_check_k(unsigned* max_err_bits) {
+    const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= (1u << 23)) return;
+    const uint32_t x = (2u * k + 1u) << 8;
+    const float e = fabsf(cheap_gumbel(x) - gumbel_from_bits(x));
+    atomicMax(max_err_bits, __float_as_uint(isfinite(e) ? e : INFINITY));
+}
+
 }  // namespace
+
+float sampler_screen_tol() { return kScreenTol; }
+
+hipError_t launch_sampler_screen_check(unsigned* d_max_err_bits, hipStream_t st) {
+    screen_check_k<<<(1 << 23) / 256, 256, 0, st>>>(d_max_err_bits);
+    return hipGetLastError();
+}
 
 hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
                          const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,

@@ -38,6 +38,40 @@ def test_sample_bitexact(rows, vocab, temp, seed, scale):
     np.testing.assert_allclose(lps.cpu().numpy(), want_lp, atol=LP_ATOL, rtol=LP_RTOL)
 
 
+def test_sampler_screening_bound_exhaustive():
+    """The cheap noise that screens vocab entries stays within the sampler's tolerance
+    of the exact noise for every one of the 2^23 values u can take (on this GPU)."""
+    err, tol = L.dash_sampler_check()
+    assert 0.0 < err and 4.0 * err <= tol, (err, tol)
+
+
+@pytest.mark.parametrize("case", ["flat", "large", "near_ties", "cold", "two_level"])
+def test_sample_screening_adversarial(case):
+    """Rows built so that many entries land close to the best score: flat logits (the
+    noise alone decides), large magnitudes (wide fp32 rounding), near-ties spaced below
+    the screening margin, a cold temperature, and a few dominant entries."""
+    rows, V = 64, 151936
+    rng = np.random.default_rng(["flat", "large", "near_ties", "cold", "two_level"].index(case))
+    temp = 1.0
+    if case == "flat":
+        logits = np.zeros((rows, V), np.float32)
+    elif case == "large":
+        logits = (3e4 + rng.standard_normal((rows, V))).astype(np.float32)
+    elif case == "near_ties":
+        logits = (rng.integers(0, 64, (rows, V)) * np.float32(2e-6)).astype(np.float32)
+    elif case == "cold":
+        logits = rng.standard_normal((rows, V)).astype(np.float32) * np.float32(0.01)
+        temp = 0.003
+    else:
+        logits = np.full((rows, V), -5.0, np.float32)
+        logits[:, rng.integers(0, V, 6)] = 8.0
+    uid = np.arange(rows, dtype=np.int32)
+    step = np.full(rows, 17, np.int32)
+    toks, _ = engine.sample(torch.from_numpy(logits).cuda(), dev_i32(uid), dev_i32(step), temp, 31)
+    want_t, _ = osm.sample(logits, uid, step, temp, 31)
+    np.testing.assert_array_equal(toks.cpu().numpy(), want_t)
+
+
 def test_sample_row_of_stride_and_nonfinite():
     V, R = 1000, 6
     wide = synth.make_logits(R, V + 24, seed=9)  # row stride 1024 > vocab
