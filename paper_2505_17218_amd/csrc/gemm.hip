@@ -284,14 +284,17 @@ __global__ void __launch_bounds__(256) gemm_f32_k(const float* __restrict__ A, c
 
 // Split-K count as a function of the weight shape only (never of M), so that a
 // row's result does not depend on how many other rows share the launch: the
-// whole path is batch-invariant, bit for bit.  Narrow outputs (few 128-column
-// tiles) are split so that a decode batch of ~1k rows still gives ~400 work items.
+// whole path is batch-invariant, bit for bit.  Only long reductions are split
+// (the down projection, K = d_ff): with 128 x 256 tiles, one workgroup per CU,
+// a decode batch of ~1k rows then gives close to one tile per CU (1.5B:
+// 8 x 6 tiles x 5 splits = 240 of 256 CUs).  Short reductions (QKV, O, K = d)
+// run unsplit on small tiles instead, which was measured faster than split-K
+// plus the partial sums it leaves for the consumer to read.
 int gemm_pick_splits(int dtype, int epi, int N, int K) {
-    if (dtype != 1 || epi != EPI_STORE_F32) return 1;
-    const int n_tiles = (N + 127) / 128;
-    if (n_tiles >= 48 || K < 512) return 1;
-    int s = (48 + n_tiles - 1) / n_tiles;
-    s = std::min(s, std::min(8, K / 256));
+    if (dtype != 1 || epi != EPI_STORE_F32 || K < 4096) return 1;
+    const int nt = (N + 255) / 256;
+    int s = std::max(1, (32 + nt / 2) / nt);  // ~32 tile-splits per 128-row block of the batch
+    s = std::min(s, std::min(8, K / 512));
     int kps = (K + s - 1) / s;
     kps = (kps + kBK - 1) / kBK * kBK;
     return (K + kps - 1) / kps;
@@ -314,6 +317,8 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         if (K >= 4096)
             return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (M <= 2048)  // decode QKV / O: unsplit, small tiles fill the GPU
+            return run_bf16<64, 64, 2, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         return run_bf16<128, 128, 4, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
     }
     if (nsplit != 1) return hipErrorInvalidValue;
