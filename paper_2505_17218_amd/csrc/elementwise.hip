@@ -11,10 +11,12 @@ namespace {
 
 constexpr int kRowThreads = 256;
 
-// One wave per row, 4 rows per workgroup; a lane holds up to kMaxV float4 of
-// the row (d <= 64 * 4 * kMaxV), so the row is read once and reduced with
-// shuffles only.
-constexpr int kMaxV = 16;
+// Row kernels (embedding + norm, residual add + norm): one workgroup of 256
+// threads per row, so even a small decode batch spreads over many CUs; a thread
+// holds up to kMaxV float4 of the row (d <= 256 * 4 * kMaxV), the row is read
+// once, and the sum of squares is reduced with shuffles and one LDS step.
+constexpr int kMaxV = 4;
+constexpr int kMaxSplits = 8;  // split-K partials summed by add_rmsnorm_k
 
 template <typename T>
 DASH_DEV void store4(T* p, float4 v);
@@ -47,9 +49,8 @@ __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __
                                                                const T* __restrict__ w, float* __restrict__ x,
                                                                T* __restrict__ y, int rows, int d, int vocab,
                                                                float eps) {
-    const int lane = threadIdx.x & 63;
-    const int r = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
-    if (r >= rows) return;
+    __shared__ float red[kRowThreads / 64];
+    const int r = blockIdx.x;
     int t = tok[r];
     t = t < 0 ? 0 : (t >= vocab ? vocab - 1 : t);  // never index outside the table
     const int d4 = d >> 2;
@@ -57,17 +58,17 @@ __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxV; ++j) {
-        const int i = lane + 64 * j;
+        const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
             v[j] = load4(E + (size_t)t * d + 4 * i);
             ss += dot4(v[j]);
         }
     }
-    ss = wave_sum(ss);
+    ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
     for (int j = 0; j < kMaxV; ++j) {
-        const int i = lane + 64 * j;
+        const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
             *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = v[j];
             const float4 g = load4(w + 4 * i);
@@ -77,36 +78,46 @@ __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __
     }
 }
 
+// Row i_out (input row r = row_map ? row_map[i_out] : i_out):
+// x[r] += sum of the nsplit partials delta[s][r] (in split order); y[i_out] =
+// RMSNorm(x[r]) * w; x is written back if write_x.
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads) add_rmsnorm_k(float* __restrict__ x, const float* __restrict__ delta,
                                                              int nsplit, size_t split_stride,
                                                              const T* __restrict__ w, T* __restrict__ y,
                                                              const int32_t* __restrict__ row_map, int rows, int d,
                                                              float eps, int write_x) {
-    const int lane = threadIdx.x & 63;
-    const int i_out = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
-    if (i_out >= rows) return;
+    __shared__ float red[kRowThreads / 64];
+    const int i_out = blockIdx.x;
     const int r = row_map ? row_map[i_out] : i_out;
     const int d4 = d >> 2;
     float4 v[kMaxV];
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxV; ++j) {
-        const int i = lane + 64 * j;
+        const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
+            // all loads of this float4 are issued before the first add
+            float4 p[kMaxSplits];
+#pragma unroll
+            for (int s = 0; s < kMaxSplits; ++s)
+                if (delta && s < nsplit)
+                    p[s] = *reinterpret_cast<const float4*>(delta + s * split_stride + (size_t)r * d + 4 * i);
             float4 a = *reinterpret_cast<const float4*>(x + (size_t)r * d + 4 * i);
-            if (delta)
-                for (int s = 0; s < nsplit; ++s)
-                    a = add4(a, *reinterpret_cast<const float4*>(delta + s * split_stride + (size_t)r * d + 4 * i));
+            float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int s = 0; s < kMaxSplits; ++s)
+                if (delta && s < nsplit) sum = s ? add4(sum, p[s]) : p[s];
+            if (delta && nsplit > 0) a = add4(a, sum);
             v[j] = a;
             ss += dot4(a);
         }
     }
-    ss = wave_sum(ss);
+    ss = block_sum(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
     for (int j = 0; j < kMaxV; ++j) {
-        const int i = lane + 64 * j;
+        const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
             if (write_x) *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = v[j];
             const float4 g = load4(w + 4 * i);
@@ -216,8 +227,8 @@ inline unsigned cdiv(size_t a, size_t b) { return (unsigned)((a + b - 1) / b); }
 hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, const void* w, float* x, void* y,
                                 int rows, int d, int vocab, float eps, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
-    if (d % 4 || d > 256 * kMaxV) return hipErrorInvalidValue;
-    const unsigned blocks = cdiv(rows, kRowThreads / 64);
+    if (d % 4 || d > kRowThreads * 4 * kMaxV) return hipErrorInvalidValue;
+    const unsigned blocks = (unsigned)rows;
     if (dtype == 1)
         embed_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(tok, (const bf16_t*)E, (const bf16_t*)w, x,
                                                                 (bf16_t*)y, rows, d, vocab, eps);
@@ -231,8 +242,8 @@ hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nspli
                               const void* w, void* y, const int32_t* row_map, int rows, int d, float eps,
                               int write_x, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
-    if (d % 4 || d > 256 * kMaxV) return hipErrorInvalidValue;
-    const unsigned blocks = cdiv(rows, kRowThreads / 64);
+    if (d % 4 || d > kRowThreads * 4 * kMaxV || nsplit > kMaxSplits) return hipErrorInvalidValue;
+    const unsigned blocks = (unsigned)rows;
     if (dtype == 1)
         add_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const bf16_t*)w,
                                                               (bf16_t*)y, row_map, rows, d, eps, write_x);

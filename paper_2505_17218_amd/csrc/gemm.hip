@@ -306,15 +306,20 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
     if (dtype == 1) {
         // Tile choice may depend on M: every configuration accumulates each output
         // element with the same chain of 32x32x16 MFMAs over k, so results do not.
+        // Small batches stream the weights: narrow tiles give enough workgroups
+        // (>= 256) to pull them from HBM at full rate.
         if (epi == EPI_SWIGLU) {
             if (nsplit != 1) return hipErrorInvalidValue;
-            return M <= 64 ? run_bf16<64, 256, 1, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st)
-                           : run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+            return M <= 256 ? run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st)
+                            : run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
         }
-        if (M <= 64)
-            return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
-        if (N >= 8192)  // LM head: many tiles, the largest tile wins
+        if (N >= 8192) {  // LM head: many tiles, the largest tile wins
+            if (M <= 64)
+                return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        }
+        if (M <= 256 || (K >= 4096 && M <= 512))
+            return run_bf16<64, 32, 2, 1, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         if (K >= 4096)
             return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         if (M <= 2048)  // decode QKV / O: unsplit, small tiles fill the GPU

@@ -108,6 +108,31 @@ def test_bf16_large_batch_gemm_tiles():
         assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype]
 
 
+# a long down-projection reduction (d_ff = 4096 >= 4096): split-K on the narrow small-batch tiles
+BF16_D = synth.Shape("bf16-ff4096", 1, 256, 4, 2, 64, 4096, 500, 1e6, synth.DT_BF16)
+
+
+@pytest.mark.parametrize("n_prompts", [10, 75, 150])
+def test_bf16_gemm_tile_regimes(n_prompts):
+    """Decode batches of 40, 300 and 600 rows select different GEMM tiles (narrow
+    small-batch tiles, 64x64, 128x256 for the split-K down projection); all match the
+    oracle, and a row's logits do not depend on the regime its batch falls in."""
+    shape = BF16_D
+    w = synth.make_weights(shape, 8)
+    wl = synth.Workload("t", shape, 150, 4, 12, 3)
+    prompts = synth.make_prompts(wl, 8)[:n_prompts]
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, n_prompts * 4, 15)
+    run = run_stepwise(model, kv, prompts, 4, 3, 1.0, 5)
+    sd = shape_dict(shape)
+    for n in sorted({0, 3, n_prompts * 2 + 1, n_prompts * 4 - 1}):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], run.tokens[n])
+        assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype], n
+    if n_prompts != 10:  # rows of the first 10 prompts: same logits as in the 40-row batch
+        small = run_stepwise(model, make_kv(model, 32, 40, 15), prompts[:10], 4, 3, 1.0, 5)
+        np.testing.assert_array_equal(small.logits[0], run.logits[0][:40])
+
+
 def test_page_size_and_batch_invariance_bf16():
     """Page size 32 vs 64 and a different batch composition give bit-identical tokens and logits."""
     shape = BF16_B
