@@ -35,6 +35,16 @@ DASH_DEV int xcd_remap(int bid, int nb) {
     return x * q + (x < r ? x : r) + j;
 }
 
+// Rotate-half RoPE of the pair (a, b) = (z_i, z_{i + hd/2}) by the angle with
+// cosine c and sine s: lo = a c - b s, hi = b c + a s.  Written as one fused
+// multiply-add over a separately rounded product, so every kernel that rotates
+// (the QKV GEMM epilogue and the standalone kernel) produces the same bits
+// whatever the compiler's contraction setting.
+DASH_DEV void rope_pair(float a, float b, float c, float s, float& lo, float& hi) {
+    lo = __builtin_fmaf(a, c, -(b * s));
+    hi = __builtin_fmaf(b, c, a * s);
+}
+
 // Element access for the two storage types (float or bfloat16 bits).
 template <typename T> DASH_DEV float ld_elem(const T* p);
 template <> DASH_DEV float ld_elem<float>(const float* p) { return *p; }

@@ -165,8 +165,8 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
         const int j = h * hd + i;
         const float a = val(j), b = val(j + half);
         const float* c_s = cs + ((size_t)r * half + i) * 2;
-        const float c = c_s[0], s = c_s[1];
-        const float lo = a * c - b * s, hi = b * c + a * s;
+        float lo, hi;
+        rope_pair(a, b, c_s[0], c_s[1], lo, hi);
         if (h < n_heads) {
             T* q = q_out + ((size_t)r * n_heads + h) * hd;
             st_elem(q + i, lo);

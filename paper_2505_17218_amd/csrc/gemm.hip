@@ -45,13 +45,14 @@ DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
 __global__ void __launch_bounds__(64 * WGM * WGN)
 gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __restrict__ C, int M, int N, int K,
-             int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride) {
+             int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride, QkvRopeArgs qa) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
     constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;  // 16-byte chunks per thread per k-step
     static_assert(A_CH >= 1 && B_CH >= 1 && BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile / thread mismatch");
     static_assert(TM >= 1 && TN >= 1, "wave tile smaller than one MFMA block");
     static_assert(EPI != EPI_SWIGLU || TN % 2 == 0, "SwiGLU pairs gate/up blocks inside a wave");
+    static_assert(EPI != EPI_QKV_ROPE || BN == 128, "the QKV epilogue works on 128-column tiles (whole heads)");
     __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * kLdsStride];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * kLdsStride];
 
@@ -131,6 +132,10 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
     };
     const int frow = lane & 31, fk = (lane >> 5) * 8;
     auto compute = [&](int buf) {
+        // let the scheduler interleave LDS reads with the MFMAs (measured: 4-10% faster,
+        // same results); the 256x256 tile keeps the variant that does not spill
+        if constexpr (BM * BN >= 256 * 256) __builtin_amdgcn_iglp_opt(1);
+        else __builtin_amdgcn_iglp_opt(0);
 #pragma unroll
         for (int ks = 0; ks < kBK; ks += 16) {
             bf16x8_t af[TM], bfr[TN];
@@ -167,7 +172,75 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
 
     // acc[i][j][r]: row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j)
     const int rbase = (lane >> 5) * 4, ccol = lane & 31;
-    if (EPI == EPI_STORE_F32) {
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        // Stage the fp32 tile in LDS (the operand tiles are dead after the loop's last
+        // barrier), then one thread per RoPE pair (q, k tiles) or v element.
+        constexpr int CS = BN + 4;
+        static_assert(BM * CS * 4 <= (int)sizeof(Bs), "C tile must fit the B operand LDS");
+        float* Cs = reinterpret_cast<float*>(&Bs[0][0]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    Cs[(wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3)) * CS + wc * WN + j * 32 + ccol] = acc[i][j][r];
+        __syncthreads();
+        const KVGeom& g = qa.g;
+        const int hd = g.head_dim, half = hd >> 1;
+        const int lg_half = hd == 128 ? 6 : 5;  // head_dim is 64 or 128
+        const int n0 = nt * BN;
+        const int q_cols = qa.n_heads * hd, k_end = q_cols + g.n_kv * hd;
+        // per row of the tile: its cache page (or -1) and key within the page, looked up once
+        __shared__ int row_page[BM], row_key[BM];
+        if (n0 >= q_cols && tid < BM) {
+            const int m = m0 + tid;
+            int page = -1, key = 0;
+            if (m < M) {
+                const int p = qa.pos[m];
+                page = kv_page_of(g, qa.page_table, qa.slot[m], p);
+                key = p % g.page_size;
+                if (page < 0 && n0 < k_end && qa.status) atomicOr(qa.status, 1u);
+            }
+            row_page[tid] = page;
+            row_key[tid] = key;
+        }
+        __syncthreads();
+        if (n0 < k_end) {
+            // one thread per RoPE pair; consecutive threads take consecutive dims of one row
+            for (int it = tid; it < BM * (BN / 2); it += NT) {
+                const int rl = it / (BN / 2), pi = it - rl * (BN / 2);
+                const int m = m0 + rl;
+                if (m >= M) continue;
+                const int hl = pi >> lg_half, i = pi & (half - 1);
+                const int c = hl * hd + i, n = n0 + c;
+                const float a = Cs[rl * CS + c] + bf2f(qa.bias[n]);
+                const float b = Cs[rl * CS + c + half] + bf2f(qa.bias[n + half]);
+                const float2 cs = *reinterpret_cast<const float2*>(qa.cs + ((size_t)m * half + i) * 2);
+                float lo, hi;
+                rope_pair(a, b, cs.x, cs.y, lo, hi);
+                if (n < q_cols) {
+                    bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + n / hd) * hd;
+                    q[i] = f2bf(lo);
+                    q[i + half] = f2bf(hi);
+                } else if (row_page[rl] >= 0) {
+                    bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) / hd, 0);
+                    kb[k_index_bf16(g, row_key[rl], i)] = f2bf(lo);
+                    kb[k_index_bf16(g, row_key[rl], i + half)] = f2bf(hi);
+                }
+            }
+        } else {
+            for (int it = tid; it < BM * BN; it += NT) {
+                const int rl = it / BN, c = it - rl * BN;
+                const int m = m0 + rl, n = n0 + c;
+                if (m >= M || n >= N || row_page[rl] < 0) continue;
+                const float v = Cs[rl * CS + c] + bf2f(qa.bias[n]);
+                const int jj = n - k_end;
+                bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
+                vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))] = f2bf(v);
+            }
+        }
+    } else if constexpr (EPI == EPI_STORE_F32) {
         float* Cp = reinterpret_cast<float*>(C) + split * split_stride;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -182,6 +255,7 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
                 }
             }
     } else {
+        static_assert(EPI == EPI_SWIGLU, "unknown epilogue");
         bf16_t* H = reinterpret_cast<bf16_t*>(C);
         const int ff = N >> 1;
 #pragma unroll
@@ -201,7 +275,7 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
 
 template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
 hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int nsplit,
-                     size_t split_stride, hipStream_t st) {
+                     size_t split_stride, hipStream_t st, const QkvRopeArgs& qa = QkvRopeArgs{}) {
     const int m_tiles = (M + BM - 1) / BM;
     const int cols = EPI == EPI_SWIGLU ? N / 2 : N;
     const int tn = EPI == EPI_SWIGLU ? BN / 2 : BN;
@@ -216,7 +290,7 @@ hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, 
     if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
     const int blocks = m_tiles * n_tiles * nsplit;
     gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI><<<blocks, 64 * WGM * WGN, 0, st>>>(
-        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride);
+        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride, qa);
     return hipGetLastError();
 }
 
@@ -298,6 +372,20 @@ int gemm_pick_splits(int dtype, int epi, int N, int K) {
     int kps = (K + s - 1) / s;
     kps = (kps + kBK - 1) / kBK * kBK;
     return (K + kps - 1) / kps;
+}
+
+bool gemm_qkv_fusable(int dtype, int n_heads, int n_kv, int head_dim) {
+    return dtype == 1 && (head_dim == 64 || head_dim == 128) && (n_heads * head_dim) % 128 == 0 &&
+           (n_kv * head_dim) % 128 == 0;
+}
+
+hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int K, const QkvRopeArgs& qa,
+                                hipStream_t st) {
+    if (M <= 0) return hipSuccess;
+    if (!gemm_qkv_fusable(1, qa.n_heads, qa.g.n_kv, qa.g.head_dim) ||
+        N != (qa.n_heads + 2 * qa.g.n_kv) * qa.g.head_dim)
+        return hipErrorInvalidValue;
+    return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(A, W, nullptr, M, N, K, 0, 1, 0, st, qa);
 }
 
 hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C, int M, int N, int K, int ldc,

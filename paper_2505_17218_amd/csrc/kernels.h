@@ -5,9 +5,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace dash {
+#include "common.h"
 
-struct KVGeom;
+namespace dash {
 
 // ---- elementwise (elementwise.hip) ----
 // x[r] = E[tok[r]] (fp32); y[r] = RMSNorm(x[r]) * w in the model dtype.
@@ -38,7 +38,23 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t st);
 hipError_t launch_iota_div(int32_t* p, int n, int div, hipStream_t st);  // p[i] = i / div
 
 // ---- GEMM (gemm.hip) ----
-enum { EPI_STORE_F32 = 0, EPI_SWIGLU = 1 };
+enum { EPI_STORE_F32 = 0, EPI_SWIGLU = 1, EPI_QKV_ROPE = 2 };
+// Arguments of the fused QKV epilogue (bf16 models): q/k/v bias, RoPE of q and k
+// (cos/sin table cs [rows][hd/2][2]), q written to q_out [rows][n_heads][hd], k and
+// v appended to the cache at pos[row] of slot[row] (status bit 0 for unbacked).
+struct QkvRopeArgs {
+    const bf16_t* bias;
+    const float* cs;
+    const int32_t* pos;
+    const int32_t* slot;
+    const int32_t* page_table;
+    bf16_t* pool;
+    KVGeom g;
+    int layer;
+    bf16_t* q_out;
+    int n_heads;
+    uint32_t* status;
+};
 // C = A[M,K] . W[N,K]^T with fp32 accumulation.
 //   EPI_STORE_F32: C fp32 (row stride ldc) ; split-K into nsplit partials at C + s*split_stride.
 //   EPI_SWIGLU:    W rows [0, N/2) are gate, [N/2, N) up; writes h[M, N/2] (model dtype, row stride ldc)
@@ -47,6 +63,13 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                        int nsplit, size_t split_stride, hipStream_t st);
 // Split-K count for a weight of N x K (independent of M: results are batch-invariant).
 int gemm_pick_splits(int dtype, int epi, int N, int K);
+// QKV projection with bias, RoPE and the KV append in the epilogue: the same values
+// as launch_gemm(EPI_STORE_F32, nsplit 1) followed by launch_qkv_rope_append, bit for
+// bit.  Available for bf16 models whose q and kv column ranges are multiples of 128
+// (a 128-column tile then holds whole heads); gemm_qkv_fusable says so.
+bool gemm_qkv_fusable(int dtype, int n_heads, int n_kv, int head_dim);
+hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int K, const QkvRopeArgs& qa,
+                                hipStream_t st);
 
 // ---- attention (attention.hip) ----
 // Decode attention over the paged cache for rows with 1 query each.  bf16: MFMA

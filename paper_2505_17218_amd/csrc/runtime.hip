@@ -632,6 +632,7 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
     const int sq = gemm_pick_splits(dt, EPI_STORE_F32, qr, d.d_model);
     const int so = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, hq);
     const int sd = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, d.d_ff);
+    const bool fuse_qkv = gemm_qkv_fusable(dt, d.n_heads, d.n_kv_heads, d.head_dim);
     // prefill is timed as one class by its caller; per-layer classes may be limited to one layer
     int cur_layer = -1;
     auto cls = [&](int c) {
@@ -648,12 +649,17 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
             DASH_HIP(launch_add_rmsnorm(dt, w.x, w.delta, sd, (size_t)rows * d.d_model, m->lw(l, 0), w.y, nullptr, rows,
                                         d.d_model, d.rms_eps, 1, st));
         }
-        {
+        if (fuse_qkv) {  // projection, bias, RoPE and the KV append in one kernel
             ProfScope ps(cls(DASH_K_GEMM_QKV), st);
-            DASH_HIP(launch_gemm(dt, EPI_STORE_F32, w.y, m->lw(l, 1), w.qkv, rows, qr, d.d_model, qr, sq,
-                                 (size_t)rows * qr, st));
-        }
-        {
+            const QkvRopeArgs qa{(const bf16_t*)m->lw(l, 2), w.cs, pos, slot, kv->d_table, (bf16_t*)kv->pool,
+                                 kv->g, l, (bf16_t*)w.q, d.n_heads, kv->d_status};
+            DASH_HIP(launch_gemm_qkv_rope(w.y, m->lw(l, 1), rows, qr, d.d_model, qa, st));
+        } else {
+            {
+                ProfScope ps(cls(DASH_K_GEMM_QKV), st);
+                DASH_HIP(launch_gemm(dt, EPI_STORE_F32, w.y, m->lw(l, 1), w.qkv, rows, qr, d.d_model, qr, sq,
+                                     (size_t)rows * qr, st));
+            }
             ProfScope ps(cls(DASH_K_ROPE), st);
             DASH_HIP(launch_qkv_rope_append(dt, w.qkv, sq, (size_t)rows * qr, m->lw(l, 2), w.cs, pos, slot,
                                             kv->d_table, kv->pool, kv->g, l, w.q, rows, d.n_heads, kv->d_status, st));
