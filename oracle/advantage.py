@@ -5,6 +5,9 @@
   group.  Eq. (3) is the single-path special case of one group holding all N
   samples.  Sec. 3.3 also names dividing by the standard deviation as a
   standard modification; the workloads here use (r - mean) / (std + eps).
+* Sec. 3.3 also names leaving sample n's own reward out of its baseline (fewer
+  samples, less bias): LOO mode, A_n = r_n - (S - r_n) / (G - 1) with S the
+  group's reward sum; as the single-path estimate it is the one-group case.
 * Sec. 3.5: samples whose advantage is small are dropped from the gradient
   update.  Reading: keep sample n iff |A_n| >= tau; the kept indices are
   reported in ascending order.  tau = 0.1 (Appendix A hyper-parameter table).
@@ -15,18 +18,21 @@ Arithmetic (so that the GPU matches bit for bit): float32 throughout, every
 operation rounded on its own; a group sum is a pairwise tree over the group
 zero-padded to a power of two, adjacent pairs first:
     mean = S(r) / G;  d = r - mean;  var = S(d*d) / (G - ddof);
-    std = sqrt(var) (0 when G - ddof <= 0);  A = d (MEAN_ONLY) or d / (std + eps).
+    std = sqrt(var) (0 when G - ddof <= 0);  A = d (MEAN_ONLY) or d / (std + eps);
+    LOO: A = r - (S(r) - r) / (G - 1)   (G >= 2).
 
 Pins (tests/test_oracle_advantage.py): closed-form values of toy groups,
 the zero-sum property, numpy's mean/std (ddof 0 and 1) as library routines, the
-single-path Eq. (3) as one group, and the closed-form kept set and expected kept
-fraction for binary rewards.
+single-path Eq. (3) as one group, the closed-form kept set and expected kept
+fraction for binary rewards; for LOO the exact fractions of toy groups, the
+identity A_LOO = G / (G - 1) (r - mean) in exact arithmetic, and r_0 - r_1 for
+pairs.
 """
 from __future__ import annotations
 
 import numpy as np
 
-MEAN_ONLY, STD_POP, STD_SAMPLE = 0, 1, 2
+MEAN_ONLY, STD_POP, STD_SAMPLE, LOO = 0, 1, 2, 3
 
 
 def pairwise_sum(v: np.ndarray) -> np.float32:
@@ -47,6 +53,12 @@ def group_advantage(r: np.ndarray, group: int, mode: int = STD_SAMPLE, eps: floa
     assert r.size % group == 0
     out = np.empty_like(r)
     G = np.float32(group)
+    if mode == LOO:
+        assert group >= 2, "the leave-one-out baseline needs at least two samples"
+        for g0 in range(0, r.size, group):
+            rg = r[g0:g0 + group]
+            out[g0:g0 + group] = rg - (pairwise_sum(rg) - rg) / np.float32(group - 1)
+        return out
     ddof = {MEAN_ONLY: 0, STD_POP: 0, STD_SAMPLE: 1}[mode]
     for g0 in range(0, r.size, group):
         rg = r[g0:g0 + group]

@@ -70,6 +70,33 @@ def test_single_path_is_one_group():
     np.testing.assert_allclose(a, r.astype(np.float64) - r.astype(np.float64).mean(), atol=1e-6)
 
 
+def test_leave_one_out_toy_groups():
+    """LOO baseline (Sec. 3.3): A_n = r_n - mean of the other samples, exact fractions."""
+    got = oa.group_advantage(np.array([1, 0, 0, 0], np.float32), 4, oa.LOO)
+    np.testing.assert_array_equal(got, np.array([1.0, -1 / 3, -1 / 3, -1 / 3], np.float32))
+    # G = 8, rewards (1, 1, 0, 1, 0, 0, 0, 0): ones get 1 - 2/7, zeros get -3/7
+    r = np.array([1, 1, 0, 1, 0, 0, 0, 0], np.float32)
+    want = np.where(r == 1, 1 - 2 / 7, -3 / 7)
+    np.testing.assert_allclose(oa.group_advantage(r, 8, oa.LOO), want, rtol=2 * 2.0 ** -24, atol=0)
+    # pairs: the baseline is the other sample (rewards on a 2^-10 grid, so every sum is exact)
+    r2 = (np.random.default_rng(3).integers(0, 1024, 40) / 1024).astype(np.float32)
+    a2 = oa.group_advantage(r2, 2, oa.LOO).reshape(20, 2)
+    rr = r2.reshape(20, 2)
+    np.testing.assert_array_equal(a2[:, 0], rr[:, 0] - rr[:, 1])
+    np.testing.assert_array_equal(a2[:, 1], rr[:, 1] - rr[:, 0])
+
+
+def test_leave_one_out_is_scaled_mean_centering():
+    """In exact arithmetic r - (S - r)/(G - 1) = G/(G - 1) (r - S/G); float32 within a few ulp."""
+    rng = np.random.default_rng(4)
+    for G in (2, 3, 5, 8, 100, 4096):
+        r = rng.random(3 * G).astype(np.float32)
+        rg = r.reshape(3, G).astype(np.float64)
+        want = G / (G - 1) * (rg - rg.mean(axis=1, keepdims=True))
+        got = oa.group_advantage(r, G, oa.LOO).reshape(3, G)
+        np.testing.assert_allclose(got, want, atol=8 * G * 2.0 ** -24)
+
+
 def test_pairwise_sum_order():
     v = np.array([1e8, 1.0, -1e8, 1.0], np.float32)
     # ((1e8 + 1) + (-1e8 + 1)) in float32 = 1e8 + -1e8 = 0
