@@ -63,7 +63,7 @@ enum { DASH_F32 = 0, DASH_BF16 = 1 };
 /* Advantage normalisation (Sec. 3.3): Eq. (4) is the group-mean baseline;
  * the std-normalised variants divide by the group std (+ eps), population
  * (ddof 0) or Bessel-corrected (ddof 1). */
-enum { DASH_ADV_MEAN_ONLY = 0, DASH_ADV_STD_POP = 1, DASH_ADV_STD_SAMPLE = 2 };
+enum { DASH_ADV_MEAN_ONLY = 0, DASH_ADV_STD_POP = 1, DASH_ADV_STD_SAMPLE = 2, DASH_ADV_LOO = 3 };
 
 /*
  * Decoder description.  The policy LM is a pre-norm decoder (the paper uses
@@ -281,14 +281,16 @@ int dash_sampler_check(double* h_max_err, double* h_tol);
  * GRPO group advantage (Sec. 3.3, Eq. (4)) and gradient filter (Sec. 3.5).
  * d_rewards: float32 [n_groups * group], group k = samples k*group .. k*group+group-1.
  * mean = S(r)/G, d = r - mean, A = d (MEAN_ONLY) or d / (sqrt(S(d*d)/(G - ddof)) + eps)
- * (std = 0 when G - ddof <= 0), where S is a pairwise sum (zero-padded to a
- * power of two, adjacent pairs first) and every float32 operation is rounded
- * on its own, so results are bit-reproducible.
+ * (std = 0 when G - ddof <= 0); DASH_ADV_LOO: the leave-one-out baseline of
+ * Sec. 3.3, A = r - (S(r) - r)/(G - 1) (eps unused).  S is a pairwise sum
+ * (zero-padded to a power of two, adjacent pairs first) and every float32
+ * operation is rounded on its own, so results are bit-reproducible.  One group
+ * of all N samples is the single-path estimate, Eq. (3).
  * Outputs: d_adv float32 [N]; d_kept_idx int32 [N] capacity, the ascending
  * indices n with |A_n| >= tau; d_kept_count int32 [1].  (tau = 0 keeps all;
  * the smallest positive float keeps exactly the nonzero advantages.)
- * DASH_EINVAL for group < 1, n_groups < 1, bad mode, eps < 0, tau < 0 or NaN;
- * DASH_ENOTSUP for group > 1024 or N > 2^24.
+ * DASH_EINVAL for group < 1 (< 2 for LOO), n_groups < 1, bad mode, eps < 0,
+ * tau < 0 or NaN; DASH_ENOTSUP for group > 65536 or N > 2^24.
  */
 int dash_group_advantage_filter(const float* d_rewards, int32_t n_groups, int32_t group, int32_t mode,
                                 float eps, float tau, float* d_adv, int32_t* d_kept_idx,

@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(HERE, "libdash.so")
 
 DASH_OK, DASH_EINVAL, DASH_ENOMEM, DASH_ECAPACITY, DASH_EDEVICE, DASH_ENOTSUP = range(6)
 DASH_F32, DASH_BF16 = 0, 1
-DASH_ADV_MEAN_ONLY, DASH_ADV_STD_POP, DASH_ADV_STD_SAMPLE = 0, 1, 2
+DASH_ADV_MEAN_ONLY, DASH_ADV_STD_POP, DASH_ADV_STD_SAMPLE, DASH_ADV_LOO = 0, 1, 2, 3
 K_CLASSES = ["prefill", "embed", "norm", "rope", "gemm_qkv", "attn", "attn_combine", "gemm_o", "gemm_gate_up",
              "gemm_down", "gemm_lm_head", "sample", "advantage", "other"]
 K = {name: i for i, name in enumerate(K_CLASSES)}

@@ -9,7 +9,12 @@
 // lanes", P2 = next power of two >= G lanes per group with the tail zero, so a
 // group sits in an aligned run of P2 lanes of one wave and an xor butterfly
 // (offsets 1, 2, 4, ...) forms the pairwise sum, adjacent pairs first.  Groups
-// with 64 < G <= 1024 use the same tree in LDS, one group at a time.
+// with 64 < G <= 1024 use the same tree in LDS, one group at a time; larger
+// groups (up to 65536, e.g. the single-path baseline over a whole batch) give
+// each thread a power-of-two run of the group, summed pairwise with a binary
+// counter, then the LDS tree over the threads: the same tree, level by level.
+// Modes: mean-centred (Eq. (4)), / (std + eps) with ddof 0 or 1, and the
+// leave-one-out baseline r - (S - r) / (G - 1).
 // Built with -ffp-contract=off: see sampler_math.h.
 #include "common.h"
 #include "kernels.h"
@@ -41,6 +46,11 @@ DASH_DEV int block_excl_scan(bool flag, int* scan, int* total) {
     return before + in_wave;
 }
 
+constexpr int kModeLoo = 3;
+
+// Leave-one-out advantage from the reward x and its group's sum S.
+DASH_DEV float adv_loo(float x, float S, int G) { return x - div_rn(S - x, (float)(G - 1)); }
+
 DASH_DEV float adv_of(float d, float ss, int G, int mode, float eps) {
     if (mode == 0) return d;
     const int ddof = mode == 2 ? 1 : 0;
@@ -66,9 +76,9 @@ __global__ void __launch_bounds__(kThreads) adv_filter_wave_k(const float* __res
         const float mu = div_rn(s, (float)G);
         const float d = x - mu;
         float q = valid ? d * d : 0.f;
-        if (mode != 0)
+        if (mode != 0 && mode != kModeLoo)
             for (int o = 1; o < P2; o <<= 1) q = q + __shfl_xor(q, o, 64);
-        const float a = adv_of(d, q, G, mode, eps);
+        const float a = mode == kModeLoo ? adv_loo(x, s, G) : adv_of(d, q, G, mode, eps);
         const bool keep = valid && fabsf(a) >= tau;
         if (valid) adv[n] = a;
         int tot;
@@ -99,7 +109,8 @@ __global__ void __launch_bounds__(kThreads) adv_filter_lds_k(const float* __rest
             if (j < half) buf[j] = t;
             __syncthreads();
         }
-        const float mu = div_rn(buf[0], (float)G);
+        const float S = buf[0];
+        const float mu = div_rn(S, (float)G);
         const float d = x - mu;
         __syncthreads();
         if (j < P2) buf[j] = valid ? d * d : 0.f;
@@ -111,7 +122,7 @@ __global__ void __launch_bounds__(kThreads) adv_filter_lds_k(const float* __rest
             if (j < half) buf[j] = t;
             __syncthreads();
         }
-        const float a = adv_of(d, buf[0], G, mode, eps);
+        const float a = mode == kModeLoo ? adv_loo(x, S, G) : adv_of(d, buf[0], G, mode, eps);
         __syncthreads();
         const bool keep = valid && fabsf(a) >= tau;
         if (valid) adv[n] = a;
@@ -119,6 +130,84 @@ __global__ void __launch_bounds__(kThreads) adv_filter_lds_k(const float* __rest
         const int at = block_excl_scan(keep, scan, &tot);
         if (keep) kept[base + at] = n;
         base += tot;
+    }
+    if (threadIdx.x == 0) *count = base;
+}
+
+constexpr int kMaxRunLog = 6;  // runs of up to 64 samples per thread: groups up to 65536
+
+// Pairwise sum of val(0 .. kThreads * c - 1) (c a power of two <= 2^kMaxRunLog):
+// thread t sums its run [t c, (t + 1) c) with a binary counter (a finished pair
+// of 2^k-sums merges left + right, as one level of the tree), then LDS adds
+// adjacent thread results level by level.  Returns the total in every thread.
+template <typename F>
+DASH_DEV float block_pairwise_sum(F val, int c, float* buf) {
+    const int t = threadIdx.x;
+    float st[kMaxRunLog];
+    float run = 0.f;
+    for (int i = 0; i < c; ++i) {
+        float v = val(t * c + i);
+        bool placed = false;
+#pragma unroll
+        for (int k = 0; k < kMaxRunLog; ++k) {
+            if (!placed) {
+                if ((i >> k) & 1) {
+                    v = st[k] + v;
+                } else {
+                    st[k] = v;
+                    placed = true;
+                }
+            }
+        }
+        run = v;  // after the last element every level has merged: the run's total
+    }
+    __syncthreads();
+    buf[t] = run;
+    __syncthreads();
+    for (int half = kThreads >> 1; half >= 1; half >>= 1) {
+        float x = 0.f;
+        if (t < half) x = buf[2 * t] + buf[2 * t + 1];
+        __syncthreads();
+        if (t < half) buf[t] = x;
+        __syncthreads();
+    }
+    const float total = buf[0];
+    __syncthreads();
+    return total;
+}
+
+__global__ void __launch_bounds__(kThreads) adv_filter_big_k(const float* __restrict__ r, int n_groups, int G, int P2,
+                                                             int mode, float eps, float tau, float* __restrict__ adv,
+                                                             int32_t* __restrict__ kept, int32_t* __restrict__ count) {
+    __shared__ float buf[kThreads];
+    __shared__ int scan[kWaves];
+    const int c = P2 / kThreads;
+    int base = 0;
+    for (int grp = 0; grp < n_groups; ++grp) {
+        const float* rg = r + (size_t)grp * G;
+        const float S = block_pairwise_sum([&](int j) { return j < G ? rg[j] : 0.f; }, c, buf);
+        const float mu = div_rn(S, (float)G);
+        float ss = 0.f;
+        if (mode != 0 && mode != kModeLoo)
+            ss = block_pairwise_sum(
+                [&](int j) {
+                    if (j >= G) return 0.f;
+                    const float d = rg[j] - mu;
+                    return d * d;
+                },
+                c, buf);
+        for (int c0 = 0; c0 < G; c0 += kThreads) {
+            const int j = c0 + threadIdx.x;
+            const bool valid = j < G;
+            const float x = valid ? rg[j] : 0.f;
+            const float a = mode == kModeLoo ? adv_loo(x, S, G) : adv_of(x - mu, ss, G, mode, eps);
+            const bool keep = valid && fabsf(a) >= tau;
+            if (valid) adv[(size_t)grp * G + j] = a;
+            int tot;
+            const int at = block_excl_scan(keep, scan, &tot);
+            if (keep) kept[base + at] = grp * G + j;
+            base += tot;
+        }
     }
     if (threadIdx.x == 0) *count = base;
 }
@@ -156,10 +245,13 @@ hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group
                                          float* adv, int32_t* kept, int32_t* count, hipStream_t st) {
     int P2 = 1;
     while (P2 < group) P2 <<= 1;
+    if (P2 > (kThreads << kMaxRunLog)) return hipErrorInvalidValue;
     if (P2 <= 64)
         adv_filter_wave_k<<<1, kThreads, 0, st>>>(r, n_groups, group, P2, mode, eps, tau, adv, kept, count);
-    else
+    else if (P2 <= kThreads)
         adv_filter_lds_k<<<1, kThreads, 0, st>>>(r, n_groups, group, P2, mode, eps, tau, adv, kept, count);
+    else
+        adv_filter_big_k<<<1, kThreads, 0, st>>>(r, n_groups, group, P2, mode, eps, tau, adv, kept, count);
     return hipGetLastError();
 }
 

@@ -900,9 +900,10 @@ int dash_group_advantage_filter(const float* r, int32_t n_groups, int32_t group,
                                 float* adv, int32_t* kept, int32_t* count, void* stream) {
     if (!r || !adv || !kept || !count) return fail(DASH_EINVAL, "dash_group_advantage_filter: NULL argument");
     if (n_groups < 1 || group < 1) return fail(DASH_EINVAL, "n_groups and group must be >= 1");
-    if (mode < DASH_ADV_MEAN_ONLY || mode > DASH_ADV_STD_SAMPLE) return fail(DASH_EINVAL, "bad mode %d", mode);
+    if (mode < DASH_ADV_MEAN_ONLY || mode > DASH_ADV_LOO) return fail(DASH_EINVAL, "bad mode %d", mode);
+    if (mode == DASH_ADV_LOO && group < 2) return fail(DASH_EINVAL, "the leave-one-out baseline needs group >= 2");
     if (!(eps >= 0.f) || !(tau >= 0.f)) return fail(DASH_EINVAL, "eps and tau must be >= 0 (and not NaN)");
-    if (group > 1024) return fail(DASH_ENOTSUP, "group > 1024");
+    if (group > 65536) return fail(DASH_ENOTSUP, "group > 65536");
     if ((int64_t)n_groups * group > (1 << 24)) return fail(DASH_ENOTSUP, "more than 2^24 samples");
     ProfScope ps(DASH_K_ADVANTAGE, (hipStream_t)stream);
     DASH_HIP(launch_group_advantage_filter(r, n_groups, group, mode, eps, tau, adv, kept, count, (hipStream_t)stream));

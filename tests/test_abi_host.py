@@ -97,15 +97,18 @@ def test_sample_and_advantage_validation():
     assert e.value.status == L.DASH_EINVAL
     # zero rows is a no-op, not an error
     L.dash_sample(0x1000, 512, 0, 512, None, 0x2000, 0x3000, 1.0, 1, 0x4000, None, None)
-    for args, want in [((0, 4), L.DASH_EINVAL), ((4, 0), L.DASH_EINVAL), ((1, 2048), L.DASH_ENOTSUP),
+    for args, want in [((0, 4), L.DASH_EINVAL), ((4, 0), L.DASH_EINVAL), ((1, 65537), L.DASH_ENOTSUP),
                        ((1 << 20, 64), L.DASH_ENOTSUP)]:
         with pytest.raises(L.DashError) as e:
             L.dash_group_advantage_filter(0x1000, args[0], args[1], 2, 1e-6, 0.1, 0x2000, 0x3000, 0x4000, None)
         assert e.value.status == want
-    for mode, eps, tau in [(3, 1e-6, 0.1), (2, -1.0, 0.1), (2, 1e-6, float("nan"))]:
+    for mode, eps, tau in [(4, 1e-6, 0.1), (-1, 1e-6, 0.1), (2, -1.0, 0.1), (2, 1e-6, float("nan"))]:
         with pytest.raises(L.DashError) as e:
             L.dash_group_advantage_filter(0x1000, 4, 4, mode, eps, tau, 0x2000, 0x3000, 0x4000, None)
         assert e.value.status == L.DASH_EINVAL
+    with pytest.raises(L.DashError) as e:  # leave-one-out needs a second sample
+        L.dash_group_advantage_filter(0x1000, 4, 1, L.DASH_ADV_LOO, 0.0, 0.1, 0x2000, 0x3000, 0x4000, None)
+    assert e.value.status == L.DASH_EINVAL
 
 
 def test_kv_sizes():

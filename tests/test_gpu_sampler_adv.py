@@ -102,9 +102,13 @@ def test_sample_deterministic_and_independent_of_batch_position():
     np.testing.assert_array_equal(a.cpu().numpy()[perm], b.cpu().numpy())
 
 
-@pytest.mark.parametrize("G", [1, 2, 3, 4, 5, 8, 16, 33, 64, 100, 1024])
-@pytest.mark.parametrize("mode", [L.DASH_ADV_MEAN_ONLY, L.DASH_ADV_STD_POP, L.DASH_ADV_STD_SAMPLE])
+@pytest.mark.parametrize("G", [1, 2, 3, 4, 5, 8, 16, 33, 64, 100, 1024, 1500, 4096, 65536])
+@pytest.mark.parametrize("mode", [L.DASH_ADV_MEAN_ONLY, L.DASH_ADV_STD_POP, L.DASH_ADV_STD_SAMPLE, L.DASH_ADV_LOO])
 def test_advantage_filter_bitexact(G, mode):
+    """Every mode and group size, from wave-sized groups to one group of 65536 (the
+    single-path baseline of Eq. (3) over a whole batch), bit-exact against the oracle."""
+    if mode == L.DASH_ADV_LOO and G == 1:
+        pytest.skip("the leave-one-out baseline needs two samples")
     n_groups = max(1, 4096 // G)
     r = synth.make_rewards(n_groups, G, "beta0.5", seed=G)
     # mix in continuous rewards so |A| lands everywhere, including near tau
