@@ -310,6 +310,46 @@ int dash_live_compact(const int32_t* d_tok, const int32_t* d_slot, const int32_t
                       int32_t* d_tok_out, int32_t* d_slot_out, int32_t* d_pos_out, int32_t* d_step_out,
                       int32_t* d_uid_out, int32_t* d_count, void* stream);
 
+/* ---- after the filter: log-probs of the kept samples and the PG loss ------ */
+
+/*
+ * Teacher-forced log-probabilities (the forward half of the policy-gradient
+ * step that follows the filter: Sec. 3.2's PG estimate needs
+ * log pi_theta(y | x) = sum_t log pi_theta(y_t | x, y_<t) for every kept
+ * sample).  d_tokens: int32 [n_seqs, seq_len], each row a prompt (first
+ * prompt_len tokens) followed by its completion.  d_logprobs: float32
+ * [n_seqs, seq_len - prompt_len]; entry (b, t) = log softmax(logits at position
+ * prompt_len - 1 + t)[d_tokens[b, prompt_len + t]] at temperature 1.
+ * The sequences are run through the prefill path (causal attention over the
+ * whole sequence, KV written to pages of slots 0 .. c-1, which must be empty
+ * and are released again) in chunks of c sequences, the largest c for which
+ * dash_teacher_forced_workspace_bytes(model, c, seq_len, prompt_len) <=
+ * ws_bytes and the pool holds c sequences.  The LM head output of a chunk is
+ * kept in the workspace (c * (seq_len - prompt_len) * vocab floats).
+ * DASH_ECAPACITY if not even one sequence fits.
+ */
+size_t dash_teacher_forced_workspace_bytes(const dash_model* model, int32_t seqs_per_chunk, int32_t seq_len,
+                                           int32_t prompt_len);
+int dash_teacher_forced_logprobs(dash_model* model, dash_kv* kv, const int32_t* d_tokens, int32_t n_seqs,
+                                 int32_t seq_len, int32_t prompt_len, float* d_logprobs, void* d_ws,
+                                 size_t ws_bytes, void* stream);
+
+/*
+ * Policy-gradient loss over the kept samples (Sec. 3.2, Eq. (2) with the
+ * group advantage of Sec. 3.3 and gradient filtering of Sec. 3.5; no 1/len
+ * weight): loss = -(1/n_total) * sum over k < *d_kept_count of
+ * A[n] * sum_{t < len[n]} lp[n][t], n = d_kept_idx[k], in float64.
+ * d_logprobs float32 [n_total, ld] (ld >= T); d_lengths int32 [n_total]
+ * (nullable: every sample has T tokens; values are clamped to [0, T]);
+ * d_adv float32 [n_total]; d_kept_idx / d_kept_count as written by
+ * dash_group_advantage_filter.  Outputs: d_loss float64 [1];
+ * d_seq_logprob float64 [n_total] (nullable): the sequence log-prob of every
+ * kept sample.  Deterministic (fixed reduction order).
+ */
+int dash_pg_loss(const float* d_logprobs, int64_t ld, int32_t T, const int32_t* d_lengths, const float* d_adv,
+                 const int32_t* d_kept_idx, const int32_t* d_kept_count, int32_t n_total, double* d_loss,
+                 double* d_seq_logprob, void* stream);
+
 /* ---- native rollout driver ---------------------------------------------- */
 
 /*

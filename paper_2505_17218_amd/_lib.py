@@ -65,6 +65,9 @@ _SIGS = {
     "dash_group_advantage_filter": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float, _P, _P,
                                               _P, _P]),
     "dash_live_compact": (C.c_int, [_P, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P, _P]),
+    "dash_teacher_forced_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32, C.c_int32]),
+    "dash_teacher_forced_logprobs": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
+    "dash_pg_loss": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, C.c_int32, _P, _P, _P]),
     "dash_rollout_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "dash_rollout": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _I32P, C.c_float, C.c_uint64,
                                _P, _P, C.c_int32, _P, C.c_size_t, _P]),
@@ -244,6 +247,22 @@ def dash_sampler_check() -> tuple[float, float]:
     err, tol = C.c_double(), C.c_double()
     _call("dash_sampler_check", C.byref(err), C.byref(tol))
     return err.value, tol.value
+
+
+def dash_teacher_forced_workspace_bytes(model: int, seqs_per_chunk: int, seq_len: int, prompt_len: int) -> int:
+    return load().dash_teacher_forced_workspace_bytes(model, seqs_per_chunk, seq_len, prompt_len)
+
+
+def dash_teacher_forced_logprobs(model: int, kv: int, d_tokens: int, n_seqs: int, seq_len: int, prompt_len: int,
+                                 d_logprobs: int, d_ws: int, ws_bytes: int, stream: int | None) -> None:
+    _call("dash_teacher_forced_logprobs", model, kv, d_tokens, n_seqs, seq_len, prompt_len, d_logprobs, d_ws,
+          ws_bytes, stream)
+
+
+def dash_pg_loss(d_logprobs: int, ld: int, T: int, d_lengths: int | None, d_adv: int, d_kept: int, d_kept_count: int,
+                 n_total: int, d_loss: int, d_seq_logprob: int | None, stream: int | None) -> None:
+    _call("dash_pg_loss", d_logprobs, ld, T, d_lengths, d_adv, d_kept, d_kept_count, n_total, d_loss, d_seq_logprob,
+          stream)
 
 
 def dash_profile_enable(class_mask: int) -> None:

@@ -239,7 +239,47 @@ live_compact_k(const int32_t* __restrict__ tok, const int32_t* __restrict__ slot
     if (threadIdx.x == 0) *count = base;
 }
 
+// Policy-gradient loss of the kept samples, float64: sample n's sequence
+// log-prob is the sum of its first len[n] token log-probs (in order), and
+// loss = -(1/n_total) sum_k A[kept[k]] * seqlp[kept[k]] with the k-sum split
+// over threads in a fixed assignment (k = t, t + kThreads, ...) and merged by a
+// pairwise LDS tree, so the result is reproducible bit for bit.
+__global__ void __launch_bounds__(kThreads)
+pg_loss_k(const float* __restrict__ lp, int64_t ld, int T, const int32_t* __restrict__ len,
+          const float* __restrict__ adv, const int32_t* __restrict__ kept, const int32_t* __restrict__ kept_count,
+          int n_total, double* __restrict__ loss, double* __restrict__ seq_lp) {
+    __shared__ double buf[kThreads];
+    const int K = *kept_count;
+    double acc = 0.0;
+    for (int k = threadIdx.x; k < K; k += kThreads) {
+        const int n = kept[k];
+        const int L = len ? min(max(len[n], 0), T) : T;
+        const float* row = lp + (int64_t)n * ld;
+        double s = 0.0;
+        for (int t = 0; t < L; ++t) s += (double)row[t];
+        if (seq_lp) seq_lp[n] = s;
+        acc += (double)adv[n] * s;
+    }
+    buf[threadIdx.x] = acc;
+    __syncthreads();
+    for (int half = kThreads >> 1; half >= 1; half >>= 1) {
+        double x = 0.0;
+        if (threadIdx.x < half) x = buf[2 * threadIdx.x] + buf[2 * threadIdx.x + 1];
+        __syncthreads();
+        if (threadIdx.x < half) buf[threadIdx.x] = x;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = -buf[0] / (double)n_total;
+}
+
 }  // namespace
+
+hipError_t launch_pg_loss(const float* lp, int64_t ld, int T, const int32_t* len, const float* adv,
+                          const int32_t* kept, const int32_t* kept_count, int n_total, double* loss, double* seq_lp,
+                          hipStream_t st) {
+    pg_loss_k<<<1, kThreads, 0, st>>>(lp, ld, T, len, adv, kept, kept_count, n_total, loss, seq_lp);
+    return hipGetLastError();
+}
 
 hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,
                                          float* adv, int32_t* kept, int32_t* count, hipStream_t st) {

@@ -118,6 +118,17 @@ hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, c
                          const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
                          int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,
                          hipStream_t st);
+// lp_out[b] = log softmax(logits row b)[y_b] with y_b = tokens[(b / per) * stride + off + b % per]
+// (rows grouped per sequence: `per` scored positions of a sequence whose tokens
+// start every `stride` entries, the first scored token at `off`); NaN for a token
+// outside [0, vocab); non-finite logits are left out of the normaliser.
+hipError_t launch_logprob_gather(const float* logits, int64_t ld, int rows, int vocab, const int32_t* tokens, int per,
+                                 int stride, int off, float* lp_out, hipStream_t st);
+// *loss = -(1/n_total) sum over kept samples n of A[n] * sum_{t < len[n]} lp[n][t] (float64);
+// seq_lp[n] (nullable) receives each kept sample's sequence log-prob.
+hipError_t launch_pg_loss(const float* lp, int64_t ld, int T, const int32_t* len, const float* adv,
+                          const int32_t* kept, const int32_t* kept_count, int n_total, double* loss, double* seq_lp,
+                          hipStream_t st);
 hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,
                                          float* adv, int32_t* kept, int32_t* count, hipStream_t st);
 hipError_t launch_live_compact(const int32_t* tok, const int32_t* slot, const int32_t* pos, const int32_t* step,

@@ -960,6 +960,112 @@ RolloutWs plan_rollout(const dash_model* m, int n_prompts, int P, int G, int max
 
 }  // namespace
 
+namespace {
+
+// Teacher-forced log-probs: the prefill plan for c sequences of L tokens, then
+// the fp32 logits of their c * (L - P) scored positions.
+struct TfWs {
+    Ws step;
+    float* logits;
+    size_t bytes;
+};
+
+TfWs plan_tf(const dash_model* m, int c, int L, int P, char* base) {
+    TfWs t{};
+    t.step = plan_ws(m, c * L, base, 0);
+    size_t off = t.step.bytes;
+    t.logits = base ? (float*)(base + off) : nullptr;
+    off = align_up(off + (size_t)c * (L - P) * m->d.vocab * 4, 256);
+    t.bytes = off;
+    return t;
+}
+
+}  // namespace
+
+size_t dash_teacher_forced_workspace_bytes(const dash_model* m, int32_t seqs_per_chunk, int32_t L, int32_t P) {
+    if (!m || seqs_per_chunk < 1 || P < 1 || L <= P) return 0;
+    return plan_tf(m, seqs_per_chunk, L, P, nullptr).bytes;
+}
+
+int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int32_t n_seqs, int32_t L,
+                                 int32_t P, float* d_lp, void* ws, size_t ws_bytes, void* stream) {
+    if (!m || !kv || !d_tokens || !d_lp || !ws) return fail(DASH_EINVAL, "dash_teacher_forced_logprobs: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (n_seqs < 1 || P < 1 || L <= P) return fail(DASH_EINVAL, "need n_seqs >= 1 and 1 <= prompt_len < seq_len");
+    if (L > kv->max_ctx) return fail(DASH_ECAPACITY, "seq_len %d exceeds max_ctx %d", L, kv->max_ctx);
+    if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
+    const hipStream_t st = (hipStream_t)stream;
+    const auto& d = m->d;
+    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    const int pps = (L + ps - 1) / ps;  // private pages per sequence
+    const int Tg = L - P;
+    // chunk: the most sequences that fit the workspace, the slots and the free pages
+    int cmax = std::min<int>(n_seqs, kv->g.max_seqs);
+    cmax = std::min<int>(cmax, (int)(kv->free_list.size() / pps));
+    if (cmax < 1) return fail(DASH_ECAPACITY, "the pool cannot hold one sequence of %d tokens", L);
+    int lo = 0, hi = cmax;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (plan_tf(m, mid, L, P, nullptr).bytes <= ws_bytes) lo = mid;
+        else hi = mid - 1;
+    }
+    const int c = lo;
+    if (c < 1)
+        return fail(DASH_ECAPACITY, "workspace too small: %zu < %zu bytes for one sequence", ws_bytes,
+                    plan_tf(m, 1, L, P, nullptr).bytes);
+    for (int j = 0; j < c; ++j)
+        if (kv->npages[j] || kv->len[j]) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
+    const TfWs t = plan_tf(m, c, L, P, (char*)ws);
+    const Ws& w = t.step;
+    std::vector<int32_t> pos, slot, gather, slots(c);
+    for (int j = 0; j < c; ++j) slots[j] = j;
+    int rc;
+    for (int s0 = 0; s0 < n_seqs; s0 += c) {
+        const int nc = std::min(c, n_seqs - s0);
+        for (int j = 0; j < nc; ++j) {
+            for (int p = 0; p < pps; ++p) kv->table[(size_t)j * mp + p] = kv_alloc_page(kv);
+            kv->npages[j] = pps;
+            kv->len[j] = L;
+        }
+        if ((rc = kv_push_rows(kv, 0, nc - 1, st))) return rc;
+        const int rows = nc * L, rows_lm = nc * Tg;
+        pos.resize(rows);
+        slot.resize(rows);
+        gather.resize(rows_lm);
+        for (int i = 0; i < rows; ++i) {
+            pos[i] = i % L;
+            slot[i] = i / L;
+        }
+        for (int i = 0; i < rows_lm; ++i) gather[i] = (i / Tg) * L + P - 1 + i % Tg;
+        if ((rc = kv_upload(kv, w.pos, pos.data(), (size_t)rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.slot, slot.data(), (size_t)rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.gather, gather.data(), (size_t)rows_lm * 4, st))) return rc;
+        const int32_t* tok = d_tokens + (size_t)s0 * L;
+        DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab,
+                                      d.rms_eps, st));
+        int sd = 1;
+        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, L, st, &sd, nullptr))) return rc;
+        // final norm of the positions that predict a completion token, then the LM head
+        DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
+                                    rows_lm, d.d_model, d.rms_eps, 0, st));
+        DASH_HIP(launch_gemm(d.dtype, EPI_STORE_F32, w.y, m->embed(), t.logits, rows_lm, d.vocab, d.d_model, d.vocab, 1,
+                             0, st));
+        DASH_HIP(launch_logprob_gather(t.logits, d.vocab, rows_lm, d.vocab, tok, Tg, L, P, d_lp + (size_t)s0 * Tg, st));
+        if ((rc = dash_kv_release(kv, slots.data(), nc))) return rc;
+    }
+    return DASH_OK;
+}
+
+int dash_pg_loss(const float* d_lp, int64_t ld, int32_t T, const int32_t* d_len, const float* d_adv,
+                 const int32_t* d_kept, const int32_t* d_kept_count, int32_t n_total, double* d_loss,
+                 double* d_seq_lp, void* stream) {
+    if (!d_lp || !d_adv || !d_kept || !d_kept_count || !d_loss) return fail(DASH_EINVAL, "dash_pg_loss: NULL argument");
+    if (T < 1 || ld < T || n_total < 1) return fail(DASH_EINVAL, "dash_pg_loss: bad sizes");
+    DASH_HIP(launch_pg_loss(d_lp, ld, T, d_len, d_adv, d_kept, d_kept_count, n_total, d_loss, d_seq_lp,
+                            (hipStream_t)stream));
+    return DASH_OK;
+}
+
 size_t dash_rollout_workspace_bytes(const dash_model* m, int32_t n_prompts, int32_t P, int32_t G, int32_t max_ctx) {
     if (!m || n_prompts < 1 || P < 1 || G < 1 || max_ctx < 1) return 0;
     return plan_rollout(m, n_prompts, P, G, max_ctx, nullptr).bytes;

@@ -165,7 +165,73 @@ __global__ void screen_check_k(unsigned* max_err_bits) {
     atomicMax(max_err_bits, __float_as_uint(isfinite(e) ? e : INFINITY));
 }
 
+// Log-probability of a given token under softmax(logits) (temperature 1), one
+// workgroup per row, with sample_k's log-normaliser computed in sample_k's order
+// (entries in groups of four with a stride of 256 groups, wave xor tree, the four
+// waves in order): on the same logits it returns sample_k's log-prob bit for bit.
+__global__ void __launch_bounds__(kThreads)
+logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ tokens,
+                 int per, int stride, int off, float* __restrict__ lp_out, int vec4) {
+    __shared__ float red_m[kThreads / 64];
+    __shared__ float red_z[kThreads / 64];
+    const int b = blockIdx.x;
+    const float* row = logits + (int64_t)b * ld;
+    float mx = -INFINITY, z = 0.f;
+    const int n4 = (vocab + 3) >> 2;
+    for (int g = threadIdx.x; g < n4; g += kThreads) {
+        float l[4];
+        if (vec4 && 4 * g + 3 < vocab) {
+            const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
+            l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (!isfinite(l[j])) continue;
+            if (l[j] > mx) {
+                z = z * __expf(mx - l[j]) + 1.0f;
+                mx = l[j];
+            } else {
+                z += __expf(l[j] - mx);
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float om = __shfl_xor(mx, o, 64), oz = __shfl_xor(z, o, 64);
+        const float nm = fmaxf(mx, om);
+        z = (mx == -INFINITY ? 0.f : z * __expf(mx - nm)) + (om == -INFINITY ? 0.f : oz * __expf(om - nm));
+        mx = nm;
+    }
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red_m[w] = mx;
+        red_z[w] = z;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int i = 1; i < kThreads / 64; ++i) {
+        const float nm = fmaxf(mx, red_m[i]);
+        z = (mx == -INFINITY ? 0.f : z * __expf(mx - nm)) + (red_m[i] == -INFINITY ? 0.f : red_z[i] * __expf(red_m[i] - nm));
+        mx = nm;
+    }
+    const int t = tokens[(int64_t)(b / per) * stride + off + b % per];
+    const float l = (t >= 0 && t < vocab) ? row[t] : NAN;
+    lp_out[b] = l - mx - logf(z);
+}
+
 }  // namespace
+
+hipError_t launch_logprob_gather(const float* logits, int64_t ld, int rows, int vocab, const int32_t* tokens, int per,
+                                 int stride, int off, float* lp_out, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    if (per < 1) return hipErrorInvalidValue;
+    const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
+    logprob_gather_k<<<rows, kThreads, 0, st>>>(logits, ld, vocab, tokens, per, stride, off, lp_out, vec4);
+    return hipGetLastError();
+}
 
 float sampler_screen_tol() { return kScreenTol; }
 

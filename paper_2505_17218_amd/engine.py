@@ -171,6 +171,33 @@ def advantage_filter(rewards: torch.Tensor, group: int, mode: int = L.DASH_ADV_S
     return adv, kept[:k]
 
 
+def teacher_forced_logprobs(model: Model, kv: KVCache, seqs: torch.Tensor, prompt_len: int,
+                            seqs_per_chunk: int = 8) -> torch.Tensor:
+    """dash_teacher_forced_logprobs: int32 [n, L] (prompt + completion) -> float32 [n, L - prompt_len]."""
+    n, Ls = seqs.shape
+    out = torch.empty((n, Ls - prompt_len), dtype=torch.float32, device=seqs.device)
+    c = max(1, min(seqs_per_chunk, n))
+    nbytes = L.dash_teacher_forced_workspace_bytes(model.handle, c, Ls, prompt_len)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=seqs.device)
+    L.dash_teacher_forced_logprobs(model.handle, kv.handle, seqs.data_ptr(), n, Ls, prompt_len, out.data_ptr(),
+                                   aligned(ws), nbytes, stream_handle())
+    return out
+
+
+def pg_loss(logprobs: torch.Tensor, adv: torch.Tensor, kept: torch.Tensor, lengths: torch.Tensor | None = None):
+    """dash_pg_loss over the kept indices: returns (float64 loss [1], float64 sequence log-probs [N])."""
+    N, T = logprobs.shape
+    dev = logprobs.device
+    cnt = torch.tensor([kept.numel()], dtype=torch.int32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    seq = torch.zeros(N, dtype=torch.float64, device=dev)
+    kept_buf = kept if kept.numel() else torch.zeros(1, dtype=torch.int32, device=dev)
+    L.dash_pg_loss(logprobs.data_ptr(), logprobs.stride(0), T, lengths.data_ptr() if lengths is not None else None,
+                   adv.data_ptr(), kept_buf.data_ptr(), cnt.data_ptr(), N, loss.data_ptr(), seq.data_ptr(),
+                   stream_handle())
+    return loss, seq
+
+
 class Rollout:
     """Reusable buffers for dash_rollout on one workload shape."""
 

@@ -38,7 +38,8 @@ def rollout_1p5b():
     toks, lps = toks.cpu().numpy().copy(), lps.cpu().numpy().copy()
     again, _ = ro.run(d_prompts, wl.temperature, seed, use_graph=False)
     torch.cuda.synchronize()
-    return dict(wl=wl, weights=weights, prompts=prompts, toks=toks, lps=lps, again=again.cpu().numpy(), seed=seed)
+    return dict(wl=wl, weights=weights, prompts=prompts, toks=toks, lps=lps, again=again.cpu().numpy(), seed=seed,
+                model=model, kv=kv)
 
 
 def test_fullsize_properties(rollout_1p5b):
@@ -71,3 +72,18 @@ def test_fullsize_sampled_sequences_match_oracle(rollout_1p5b, n):
         g = osm.noise(r["seed"], n, int(t), wl.shape.vocab).astype(np.float64)
         s = l64 + g
         assert s[tok] >= s.max() - 2 * LOGIT_TOL, (n, t)
+
+
+def test_fullsize_teacher_forced_recompute(rollout_1p5b):
+    """Teacher-forced log-probs of three full 1280-token sequences (prefill path, LM head
+    over every completion position) reproduce the log-probs recorded while sampling bit
+    for bit (the contexts fit the cache's single 2048-key attention split)."""
+    r = rollout_1p5b
+    wl = r["wl"]
+    P, G = wl.prompt_len, wl.group
+    ns = [0, 777, 1023]
+    seqs = np.concatenate([r["prompts"][[n // G for n in ns]], r["toks"][ns]], axis=1).astype(np.int32)
+    rec = engine.teacher_forced_logprobs(r["model"], r["kv"], torch.from_numpy(seqs).cuda(), P).cpu().numpy()
+    assert np.isfinite(rec).all()
+    assert P + wl.gen_len <= r["kv"].split_keys
+    np.testing.assert_array_equal(rec.view(np.uint32), r["lps"][ns].view(np.uint32))
