@@ -87,3 +87,37 @@ def test_fullsize_teacher_forced_recompute(rollout_1p5b):
     assert np.isfinite(rec).all()
     assert P + wl.gen_len <= r["kv"].split_keys
     np.testing.assert_array_equal(rec.view(np.uint32), r["lps"][ns].view(np.uint32))
+
+
+@pytest.mark.parametrize("workload,ns,ts", [("0.5b-b512", [0, 301, 511], [0, 1, 255, 1023]),
+                                            ("3b-b64", [0, 63], [0, 511, 1023])])
+def test_other_workloads_sampled_against_oracle(workload, ns, ts):
+    """The 0.5B (512 sequences) and 3B (64 sequences, prompt 512) workloads at full size:
+    sampled positions of sampled sequences against the oracle, as for the 1.5B run."""
+    require_gpu()
+    wl = synth.WORKLOADS[workload]
+    s = wl.shape
+    weights = synth.make_weights(s, 0)
+    prompts = synth.make_prompts(wl, 0)
+    model = engine.Model(s, weights)
+    N, P, T, ps = wl.n_seqs, wl.prompt_len, wl.gen_len, 32
+    pages = wl.n_prompts * (P // ps) + N * ((P + T + ps - 1) // ps - P // ps) + 8
+    kv = engine.KVCache(model, ps, N, P + T, pages)
+    ro = engine.Rollout(model, kv, wl.n_prompts, P, wl.group, T)
+    seed = synth.sampler_seed(0)
+    toks, lps = ro.run(torch.from_numpy(prompts).cuda(), wl.temperature, seed)
+    torch.cuda.synchronize()
+    toks, lps = toks.cpu().numpy(), lps.cpu().numpy()
+    assert ((toks >= 0) & (toks < s.vocab)).all() and np.isfinite(lps).all()
+    ts = np.array(ts)
+    for n in ns:
+        seq = np.concatenate([prompts[n // wl.group], toks[n][:ts.max()]])
+        ref = om.forward(shape_dict(s), weights, seq, positions=P - 1 + ts)
+        for i, t in enumerate(ts):
+            l64 = ref[i]
+            lse = l64.max() + np.log(np.exp(l64 - l64.max()).sum())
+            tok = int(toks[n, t])
+            assert abs((l64[tok] - lse) - lps[n, t]) <= LP_TOL, (workload, n, t)
+            g = osm.noise(seed, n, int(t), s.vocab).astype(np.float64)
+            sc = l64 + g
+            assert sc[tok] >= sc.max() - 2 * LOGIT_TOL, (workload, n, t)
