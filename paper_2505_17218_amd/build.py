@@ -1,9 +1,11 @@
 """Build libdash.so (the HIP kernels and the C ABI of include/dash.h) for gfx950.
 
 Usage: python -m paper_2505_17218_amd.build   (or __graft_entry__.build()).
-Compiles every source in csrc/ with hipcc into one shared library next to this
-file.  The sampler and advantage kernels are built with -ffp-contract=off: their
-float32 arithmetic is part of a bit-exact contract.
+Compiles every library source in csrc/ with hipcc into one shared library next to
+this file, and the native benchmark (csrc/native_bench.hip, a C-ABI client that
+needs no Python) into dash_native_bench beside it.  The sampler and advantage
+kernels are built with -ffp-contract=off: their float32 arithmetic is part of a
+bit-exact contract.
 """
 from __future__ import annotations
 
@@ -17,6 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libdash.so")
+NATIVE_BENCH = os.path.join(HERE, "dash_native_bench")
 BUILD = os.path.join(ROOT, "_build")
 
 SOURCES = ["runtime.hip", "elementwise.hip", "gemm.hip", "attention.hip", "sampler.hip", "advantage.hip"]
@@ -55,8 +58,15 @@ def build(verbose: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    tmp = NATIVE_BENCH + ".tmp"
+    cmd = [hipcc(), *COMMON, "-ffp-contract=fast", os.path.join(CSRC, "native_bench.hip"), "-o", tmp,
+           "-L", HERE, "-ldash", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"native benchmark build failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, NATIVE_BENCH)
     if verbose:
-        print(f"built {LIB}", file=sys.stderr)
+        print(f"built {LIB} and {NATIVE_BENCH}", file=sys.stderr)
     return LIB
 
 
