@@ -133,6 +133,28 @@ def test_bf16_gemm_tile_regimes(n_prompts):
         np.testing.assert_array_equal(small.logits[0], run.logits[0][:40])
 
 
+# d_ff = 2240 (35 SwiGLU tile columns of 64): a 1024-row decode batch runs gate/up on
+# 128x128 tiles with a partial last round, a 40-row batch on 64x64 tiles
+BF16_E = synth.Shape("bf16-ff2240", 1, 256, 4, 2, 64, 2240, 500, 1e6, synth.DT_BF16)
+
+
+def test_bf16_swiglu_tile_regimes_bitexact():
+    """1024 decode rows (128x128 SwiGLU tiles) give every row the same logits, bit for bit,
+    as a 40-row batch (64x64 tiles), and match the oracle."""
+    shape = BF16_E
+    w = synth.make_weights(shape, 9)
+    wl = synth.Workload("t", shape, 256, 4, 10, 2)
+    prompts = synth.make_prompts(wl, 9)
+    model = engine.Model(shape, w)
+    big = run_stepwise(model, make_kv(model, 32, 1024, 12), prompts, 4, 2, 1.0, 5)
+    small = run_stepwise(model, make_kv(model, 32, 40, 12), prompts[:10], 4, 2, 1.0, 5)
+    np.testing.assert_array_equal(small.logits[1], big.logits[1][:40])  # the decode step (M = 1024 vs 40)
+    sd = shape_dict(shape)
+    for n in (0, 511, 1023):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], big.tokens[n])
+        assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
+
+
 def test_page_size_and_batch_invariance_bf16():
     """Page size 32 vs 64 and a different batch composition give bit-identical tokens and logits."""
     shape = BF16_B
