@@ -111,6 +111,36 @@ def test_sample_and_advantage_validation():
     assert e.value.status == L.DASH_EINVAL
 
 
+def test_recompute_loss_and_profiler_validation():
+    d = _desc()
+    h = L.dash_model_create(d, _fake_ptrs(d))
+    # workspace of the teacher-forced recompute grows with the chunk; 0 for bad sizes
+    w1 = L.dash_teacher_forced_workspace_bytes(h, 1, 48, 16)
+    w4 = L.dash_teacher_forced_workspace_bytes(h, 4, 48, 16)
+    assert 0 < w1 < w4
+    assert w4 >= 4 * 32 * d.vocab * 4  # the chunk's logits: 4 sequences x 32 scored positions
+    assert L.dash_teacher_forced_workspace_bytes(h, 1, 16, 16) == 0  # nothing to score
+    assert L.dash_teacher_forced_workspace_bytes(h, 0, 48, 16) == 0
+    with pytest.raises(L.DashError) as e:  # no kv handle
+        L.dash_teacher_forced_logprobs(h, None, 0x1000, 2, 48, 16, 0x2000, 0x3000, w1, None)
+    assert e.value.status == L.DASH_EINVAL
+    L.dash_model_destroy(h)
+    for args in [(None, 8, 8, None, 0x2000, 0x3000, 0x4000, 4, 0x5000, None),   # no log-probs
+                 (0x1000, 4, 8, None, 0x2000, 0x3000, 0x4000, 4, 0x5000, None),  # ld < T
+                 (0x1000, 8, 0, None, 0x2000, 0x3000, 0x4000, 4, 0x5000, None),  # T = 0
+                 (0x1000, 8, 8, None, 0x2000, 0x3000, 0x4000, 0, 0x5000, None)]:  # n_total = 0
+        with pytest.raises(L.DashError) as e:
+            L.dash_pg_loss(*args, None)
+        assert e.value.status == L.DASH_EINVAL
+    with pytest.raises(L.DashError) as e:
+        L.dash_profile_layer(-2)
+    assert e.value.status == L.DASH_EINVAL
+    L.dash_profile_layer(-1)
+    with pytest.raises(L.DashError) as e:
+        L.dash_kv_split_keys(None)
+    assert e.value.status == L.DASH_EINVAL
+
+
 def test_kv_sizes():
     d = _desc()
     h = L.dash_model_create(d, _fake_ptrs(d))
