@@ -12,6 +12,10 @@ the rollouts use:
   counter-based Philox4x32-10 noise (float32, bit-exact contract).
 * :mod:`oracle.advantage` — the GRPO group advantage (Sec. 3.3, Eq. (4)) and
   the gradient filter (Sec. 3.5), float32, bit-exact contract.
+* :mod:`oracle.pg`        — teacher-forced log-probs of sampled completions and
+  the policy-gradient loss over the kept samples (Sec. 3.2, Eq. (2)).
+* :mod:`oracle.policy`    — the KL regulariser D_KL(pi_base || pi_theta) and the
+  clipped PPO surrogate with sequence ratios (Sec. 3.2), float64.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP path
