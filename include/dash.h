@@ -350,6 +350,61 @@ int dash_pg_loss(const float* d_logprobs, int64_t ld, int32_t T, const int32_t* 
                  const int32_t* d_kept_idx, const int32_t* d_kept_count, int32_t n_total, double* d_loss,
                  double* d_seq_logprob, void* stream);
 
+/*
+ * KL regulariser (Sec. 3.2: the divergence D_KL(pi_base || pi_theta) from the
+ * original model, weighted by beta).  Per row pair of float32 logits
+ * d_theta / d_base [rows, ld] (ld >= vocab; entries past vocab are ignored):
+ * d_kl[r] = D_KL(softmax(base_r) || softmax(theta_r)) and, if d_kl_rev is not
+ * NULL, d_kl_rev[r] = D_KL(softmax(theta_r) || softmax(base_r)), float32, at
+ * temperature 1.  A -inf logit has probability zero; an entry with mass on one
+ * side and -inf on the other makes that direction +inf; NaN logits give NaN.
+ * Exponentials in float32, sums in float64: identical rows give exactly 0.
+ */
+int dash_logits_kl(const float* d_theta, const float* d_base, int64_t ld, int32_t rows, int32_t vocab, float* d_kl,
+                   float* d_kl_rev, void* stream);
+
+/*
+ * Teacher-forced KL along sampled completions: for every completion position of
+ * d_tokens (layout as in dash_teacher_forced_logprobs), the exact KL between the
+ * next-token distributions of the base model and the policy after the same
+ * prefix, summed later over positions by dash_policy_loss.  base must have the
+ * policy's architecture (same dash_model_desc values); kv belongs to model and
+ * serves both forwards (the base model's pass runs first, slots 0 .. c-1 must
+ * be empty and are released).  Outputs float32 [n_seqs, seq_len - prompt_len]:
+ * d_logprobs (nullable; bit-identical to dash_teacher_forced_logprobs), d_kl
+ * (D_KL(base || policy)), d_kl_rev (nullable, D_KL(policy || base)).  Chunks of
+ * c sequences, the largest c with dash_teacher_forced_kl_workspace_bytes(model,
+ * c, seq_len, prompt_len) <= ws_bytes (two logits buffers per chunk).
+ */
+size_t dash_teacher_forced_kl_workspace_bytes(const dash_model* model, int32_t seqs_per_chunk, int32_t seq_len,
+                                              int32_t prompt_len);
+int dash_teacher_forced_kl(dash_model* model, dash_model* base, dash_kv* kv, const int32_t* d_tokens, int32_t n_seqs,
+                           int32_t seq_len, int32_t prompt_len, float* d_logprobs, float* d_kl, float* d_kl_rev,
+                           void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * Regularised policy loss over the kept samples (Sec. 3.2), float64.  With
+ * S_n = sum_{t < len[n]} lp[n][t]:
+ *   d_logprobs_old == NULL: surrogate_n = A_n S_n (the PG loss of dash_pg_loss);
+ *   otherwise PPO with the whole-trajectory ratio rho_n = exp(S_n - S_old,n)
+ *   (the ratio Sec. 3.2 writes) and the clipped surrogate
+ *   min(rho_n A_n, clip(rho_n, 1 - clip_eps, 1 + clip_eps) A_n), clip_eps in [0, 1).
+ * loss = -(1/n_total) sum_kept surrogate_n + (beta/n_total) sum_kept KL_n, where
+ * KL_n sums d_kl[n][t] over t < len[n] (d_kl NULL: no KL term, beta unused).
+ * d_logprobs, d_logprobs_old and d_kl are float32 [n_total, ld] (ld >= T);
+ * d_lengths, d_adv, d_kept_idx, d_kept_count as for dash_pg_loss.  Outputs:
+ * d_loss float64 [1]; d_stats float64 [n_total, 4] (nullable), for each kept n:
+ * (S_n, S_old,n (= S_n without old log-probs), KL_n, d loss / d S_n), the last
+ * being the weight a backward pass puts on grad S_n: -A_n/n_total (PG),
+ * -A_n rho_n/n_total where the unclipped term is the minimum (PPO), else 0.
+ * Deterministic; with d_logprobs_old and d_kl NULL the loss equals
+ * dash_pg_loss's bit for bit.
+ */
+int dash_policy_loss(const float* d_logprobs, const float* d_logprobs_old, const float* d_kl, int64_t ld, int32_t T,
+                     const int32_t* d_lengths, const float* d_adv, const int32_t* d_kept_idx,
+                     const int32_t* d_kept_count, int32_t n_total, double clip_eps, double beta, double* d_loss,
+                     double* d_stats, void* stream);
+
 /* ---- native rollout driver ---------------------------------------------- */
 
 /*

@@ -68,6 +68,12 @@ _SIGS = {
     "dash_teacher_forced_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32, C.c_int32]),
     "dash_teacher_forced_logprobs": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
     "dash_pg_loss": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, C.c_int32, _P, _P, _P]),
+    "dash_policy_loss": (C.c_int, [_P, _P, _P, C.c_int64, C.c_int32, _P, _P, _P, _P, C.c_int32, C.c_double,
+                                   C.c_double, _P, _P, _P]),
+    "dash_logits_kl": (C.c_int, [_P, _P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P]),
+    "dash_teacher_forced_kl_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32, C.c_int32]),
+    "dash_teacher_forced_kl": (C.c_int, [_P, _P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P, _P,
+                                         C.c_size_t, _P]),
     "dash_rollout_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "dash_rollout": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _I32P, C.c_float, C.c_uint64,
                                _P, _P, C.c_int32, _P, C.c_size_t, _P]),
@@ -263,6 +269,29 @@ def dash_pg_loss(d_logprobs: int, ld: int, T: int, d_lengths: int | None, d_adv:
                  n_total: int, d_loss: int, d_seq_logprob: int | None, stream: int | None) -> None:
     _call("dash_pg_loss", d_logprobs, ld, T, d_lengths, d_adv, d_kept, d_kept_count, n_total, d_loss, d_seq_logprob,
           stream)
+
+
+def dash_policy_loss(d_logprobs: int, d_logprobs_old: int | None, d_kl: int | None, ld: int, T: int,
+                     d_lengths: int | None, d_adv: int, d_kept: int, d_kept_count: int, n_total: int,
+                     clip_eps: float, beta: float, d_loss: int, d_stats: int | None, stream: int | None) -> None:
+    _call("dash_policy_loss", d_logprobs, d_logprobs_old, d_kl, ld, T, d_lengths, d_adv, d_kept, d_kept_count,
+          n_total, C.c_double(clip_eps), C.c_double(beta), d_loss, d_stats, stream)
+
+
+def dash_logits_kl(d_theta: int, d_base: int, ld: int, rows: int, vocab: int, d_kl: int, d_kl_rev: int | None,
+                   stream: int | None) -> None:
+    _call("dash_logits_kl", d_theta, d_base, ld, rows, vocab, d_kl, d_kl_rev, stream)
+
+
+def dash_teacher_forced_kl_workspace_bytes(model: int, seqs_per_chunk: int, seq_len: int, prompt_len: int) -> int:
+    return load().dash_teacher_forced_kl_workspace_bytes(model, seqs_per_chunk, seq_len, prompt_len)
+
+
+def dash_teacher_forced_kl(model: int, base: int, kv: int, d_tokens: int, n_seqs: int, seq_len: int, prompt_len: int,
+                           d_logprobs: int | None, d_kl: int, d_kl_rev: int | None, d_ws: int, ws_bytes: int,
+                           stream: int | None) -> None:
+    _call("dash_teacher_forced_kl", model, base, kv, d_tokens, n_seqs, seq_len, prompt_len, d_logprobs, d_kl,
+          d_kl_rev, d_ws, ws_bytes, stream)
 
 
 def dash_profile_enable(class_mask: int) -> None:

@@ -244,41 +244,97 @@ live_compact_k(const int32_t* __restrict__ tok, const int32_t* __restrict__ slot
 // loss = -(1/n_total) sum_k A[kept[k]] * seqlp[kept[k]] with the k-sum split
 // over threads in a fixed assignment (k = t, t + kThreads, ...) and merged by a
 // pairwise LDS tree, so the result is reproducible bit for bit.
+// Loss over the kept samples, float64.  Each thread takes kept samples k, k + 256, ...
+// and sums a sample's per-token values in token order; the 256 partials are then
+// added as a pairwise tree.  Surrogate: A S (PG, no old log-probs) or PPO's
+// min(rho A, clip(rho, 1 - eps, 1 + eps) A) with rho = exp(S - S_old); the KL sums
+// (if given) enter with weight beta.  stats[4 n ..] = (S, S_old, KL, dloss/dS).
 __global__ void __launch_bounds__(kThreads)
-pg_loss_k(const float* __restrict__ lp, int64_t ld, int T, const int32_t* __restrict__ len,
-          const float* __restrict__ adv, const int32_t* __restrict__ kept, const int32_t* __restrict__ kept_count,
-          int n_total, double* __restrict__ loss, double* __restrict__ seq_lp) {
-    __shared__ double buf[kThreads];
+policy_loss_k(const float* __restrict__ lp, const float* __restrict__ lp_old, const float* __restrict__ kl, int64_t ld,
+              int T, const int32_t* __restrict__ len, const float* __restrict__ adv,
+              const int32_t* __restrict__ kept, const int32_t* __restrict__ kept_count, int n_total, double clip_eps,
+              double beta, double* __restrict__ loss, double* __restrict__ seq_lp, double* __restrict__ stats) {
+    __shared__ double buf[kThreads], kbuf[kThreads];
     const int K = *kept_count;
-    double acc = 0.0;
+    const double N = (double)n_total;
+    double acc = 0.0, kacc = 0.0;
     for (int k = threadIdx.x; k < K; k += kThreads) {
         const int n = kept[k];
         const int L = len ? min(max(len[n], 0), T) : T;
         const float* row = lp + (int64_t)n * ld;
-        double s = 0.0;
-        for (int t = 0; t < L; ++t) s += (double)row[t];
-        if (seq_lp) seq_lp[n] = s;
-        acc += (double)adv[n] * s;
+        double S = 0.0;
+        for (int t = 0; t < L; ++t) S += (double)row[t];
+        double S_old = S, Kn = 0.0;
+        if (lp_old) {
+            const float* ro = lp_old + (int64_t)n * ld;
+            S_old = 0.0;
+            for (int t = 0; t < L; ++t) S_old += (double)ro[t];
+        }
+        if (kl) {
+            const float* rk = kl + (int64_t)n * ld;
+            for (int t = 0; t < L; ++t) Kn += (double)rk[t];
+        }
+        const double A = (double)adv[n];
+        double sur, w;
+        if (!lp_old) {
+            sur = A * S;
+            w = -A / N;
+        } else {
+            const double rho = exp(S - S_old);
+            const double un = rho * A;
+            const double cl = fmin(fmax(rho, 1.0 - clip_eps), 1.0 + clip_eps) * A;
+            sur = fmin(un, cl);
+            w = un <= cl ? -A * rho / N : 0.0;
+        }
+        if (seq_lp) seq_lp[n] = S;
+        if (stats) {
+            stats[4 * (int64_t)n + 0] = S;
+            stats[4 * (int64_t)n + 1] = S_old;
+            stats[4 * (int64_t)n + 2] = Kn;
+            stats[4 * (int64_t)n + 3] = w;
+        }
+        acc += sur;
+        kacc += Kn;
     }
     buf[threadIdx.x] = acc;
+    kbuf[threadIdx.x] = kacc;
     __syncthreads();
     for (int half = kThreads >> 1; half >= 1; half >>= 1) {
-        double x = 0.0;
-        if (threadIdx.x < half) x = buf[2 * threadIdx.x] + buf[2 * threadIdx.x + 1];
+        double x = 0.0, y = 0.0;
+        if (threadIdx.x < half) {
+            x = buf[2 * threadIdx.x] + buf[2 * threadIdx.x + 1];
+            y = kbuf[2 * threadIdx.x] + kbuf[2 * threadIdx.x + 1];
+        }
         __syncthreads();
-        if (threadIdx.x < half) buf[threadIdx.x] = x;
+        if (threadIdx.x < half) {
+            buf[threadIdx.x] = x;
+            kbuf[threadIdx.x] = y;
+        }
         __syncthreads();
     }
-    if (threadIdx.x == 0) *loss = -buf[0] / (double)n_total;
+    if (threadIdx.x == 0) {
+        double l = -buf[0] / N;
+        if (kl) l += beta * kbuf[0] / N;
+        *loss = l;
+    }
 }
 
 }  // namespace
 
+hipError_t launch_policy_loss(const float* lp, const float* lp_old, const float* kl, int64_t ld, int T,
+                              const int32_t* len, const float* adv, const int32_t* kept, const int32_t* kept_count,
+                              int n_total, double clip_eps, double beta, double* loss, double* seq_lp, double* stats,
+                              hipStream_t st) {
+    policy_loss_k<<<1, kThreads, 0, st>>>(lp, lp_old, kl, ld, T, len, adv, kept, kept_count, n_total, clip_eps, beta,
+                                          loss, seq_lp, stats);
+    return hipGetLastError();
+}
+
 hipError_t launch_pg_loss(const float* lp, int64_t ld, int T, const int32_t* len, const float* adv,
                           const int32_t* kept, const int32_t* kept_count, int n_total, double* loss, double* seq_lp,
                           hipStream_t st) {
-    pg_loss_k<<<1, kThreads, 0, st>>>(lp, ld, T, len, adv, kept, kept_count, n_total, loss, seq_lp);
-    return hipGetLastError();
+    return launch_policy_loss(lp, nullptr, nullptr, ld, T, len, adv, kept, kept_count, n_total, 0.0, 0.0, loss, seq_lp,
+                              nullptr, st);
 }
 
 hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,

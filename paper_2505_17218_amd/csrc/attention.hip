@@ -173,10 +173,12 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
     constexpr int ND = HD / 16;
     const int lane = threadIdx.x;
     const int n_kv = g.n_kv;
-    // work items (row, kv head) fastest, split slowest, dealt to XCDs in contiguous
-    // runs: the rows of one prompt group read their shared prompt pages through one L2
+    // work items: split fastest, then kv head, then row, dealt to XCDs in contiguous
+    // runs.  Every XCD gets whole rows with all their splits (the splits past a short
+    // context, which exit at once, are spread evenly instead of filling the last XCDs),
+    // and the rows of one prompt group read their shared prompt pages through one L2.
     const int wi = xcd_remap(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
-    const int rk = wi % gridDim.x, split = wi / gridDim.x;
+    const int rk = wi / gridDim.y, split = wi % gridDim.y;
     const int row = rk / n_kv, kvh = rk % n_kv;
     const int rep = n_heads / n_kv;
     const int head = lane & 15, grp = lane >> 4;

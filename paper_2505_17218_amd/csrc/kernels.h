@@ -124,11 +124,23 @@ hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, c
 // outside [0, vocab); non-finite logits are left out of the normaliser.
 hipError_t launch_logprob_gather(const float* logits, int64_t ld, int rows, int vocab, const int32_t* tokens, int per,
                                  int stride, int off, float* lp_out, hipStream_t st);
+// Per row pair: D_KL(softmax(base) || softmax(theta)) into kl and the reverse
+// direction into kl_rev (may be null); -inf logits have probability zero.
+hipError_t launch_logits_kl(const float* theta, const float* base, int64_t ld, int rows, int vocab, float* kl,
+                            float* kl_rev, hipStream_t st);
 // *loss = -(1/n_total) sum over kept samples n of A[n] * sum_{t < len[n]} lp[n][t] (float64);
 // seq_lp[n] (nullable) receives each kept sample's sequence log-prob.
 hipError_t launch_pg_loss(const float* lp, int64_t ld, int T, const int32_t* len, const float* adv,
                           const int32_t* kept, const int32_t* kept_count, int n_total, double* loss, double* seq_lp,
                           hipStream_t st);
+// The general form: surrogate A S, or PPO's clipped min(rho A, clip(rho, 1 +- eps) A)
+// with rho = exp(S - S_old) when lp_old is given; plus (beta / n_total) times the
+// kept KL sums when kl is given.  lp, lp_old and kl share the row stride ld.
+// stats[4 n ..] (nullable) = (S, S_old, KL sum, d loss / d S) of each kept n.
+hipError_t launch_policy_loss(const float* lp, const float* lp_old, const float* kl, int64_t ld, int T,
+                              const int32_t* len, const float* adv, const int32_t* kept, const int32_t* kept_count,
+                              int n_total, double clip_eps, double beta, double* loss, double* seq_lp, double* stats,
+                              hipStream_t st);
 hipError_t launch_group_advantage_filter(const float* r, int n_groups, int group, int mode, float eps, float tau,
                                          float* adv, int32_t* kept, int32_t* count, hipStream_t st);
 hipError_t launch_live_compact(const int32_t* tok, const int32_t* slot, const int32_t* pos, const int32_t* step,

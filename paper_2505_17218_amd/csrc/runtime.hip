@@ -678,9 +678,11 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
                     DASH_HIP(launch_decode_attention(dt, w.q, pos, slot, kv->d_table, kv->pool, kv->g, l, d.n_heads,
                                                      w.o, rows, kv->max_ctx, w.attn_part, st));
             }
-            ProfScope ps(cls(DASH_K_ATTN_COMBINE), st);
-            DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, kv->g.split_keys,
-                                              w.attn_part, w.o, st));
+            if (dt == DASH_BF16 && kv->max_ctx > kv->g.split_keys) {  // the combine launches only for several splits
+                ProfScope ps(cls(DASH_K_ATTN_COMBINE), st);
+                DASH_HIP(launch_attention_combine(dt, pos, rows, d.n_heads, d.head_dim, kv->max_ctx, kv->g.split_keys,
+                                                  w.attn_part, w.o, st));
+            }
         }
         {
             ProfScope ps(cls(DASH_K_GEMM_O), st);
@@ -980,6 +982,50 @@ TfWs plan_tf(const dash_model* m, int c, int L, int P, char* base) {
     return t;
 }
 
+// Forward of a chunk of whole sequences (rows = sequences x L tokens, positions,
+// slots and gather rows already uploaded to w, pages mapped) through model m on
+// kv's pages; the LM head writes the logits of the rows_lm gathered positions.
+int tf_forward(dash_model* m, dash_kv* kv, const Ws& w, const int32_t* tok, int rows, int rows_lm, int L,
+               float* logits, hipStream_t st) {
+    const auto& d = m->d;
+    DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab, d.rms_eps,
+                                  st));
+    int sd = 1, rc;
+    if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, L, st, &sd, nullptr))) return rc;
+    // final norm of the positions that predict a completion token, then the LM head
+    DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
+                                rows_lm, d.d_model, d.rms_eps, 0, st));
+    DASH_HIP(launch_gemm(d.dtype, EPI_STORE_F32, w.y, m->embed(), logits, rows_lm, d.vocab, d.d_model, d.vocab, 1, 0,
+                         st));
+    return DASH_OK;
+}
+
+// Teacher-forced KL workspace: the step buffers plus logits of both models.
+struct TfKlWs {
+    Ws step;
+    float* logits;
+    float* logits_base;
+    size_t bytes;
+};
+
+TfKlWs plan_tf_kl(const dash_model* m, int c, int L, int P, char* base) {
+    TfKlWs t{};
+    t.step = plan_ws(m, c * L, base, 0);
+    const size_t lb = (size_t)c * (L - P) * m->d.vocab * 4;
+    size_t off = t.step.bytes;
+    t.logits = base ? (float*)(base + off) : nullptr;
+    off = align_up(off + lb, 256);
+    t.logits_base = base ? (float*)(base + off) : nullptr;
+    t.bytes = align_up(off + lb, 256);
+    return t;
+}
+
+bool same_architecture(const dash_model_desc& a, const dash_model_desc& b) {
+    return a.n_layers == b.n_layers && a.d_model == b.d_model && a.n_heads == b.n_heads &&
+           a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim && a.d_ff == b.d_ff && a.vocab == b.vocab &&
+           a.dtype == b.dtype && a.rope_theta == b.rope_theta && a.rms_eps == b.rms_eps;
+}
+
 }  // namespace
 
 size_t dash_teacher_forced_workspace_bytes(const dash_model* m, int32_t seqs_per_chunk, int32_t L, int32_t P) {
@@ -1041,15 +1087,7 @@ int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_to
         if ((rc = kv_upload(kv, w.slot, slot.data(), (size_t)rows * 4, st))) return rc;
         if ((rc = kv_upload(kv, w.gather, gather.data(), (size_t)rows_lm * 4, st))) return rc;
         const int32_t* tok = d_tokens + (size_t)s0 * L;
-        DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab,
-                                      d.rms_eps, st));
-        int sd = 1;
-        if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, L, st, &sd, nullptr))) return rc;
-        // final norm of the positions that predict a completion token, then the LM head
-        DASH_HIP(launch_add_rmsnorm(d.dtype, w.x, w.delta, sd, (size_t)rows * d.d_model, m->final_norm(), w.y, w.gather,
-                                    rows_lm, d.d_model, d.rms_eps, 0, st));
-        DASH_HIP(launch_gemm(d.dtype, EPI_STORE_F32, w.y, m->embed(), t.logits, rows_lm, d.vocab, d.d_model, d.vocab, 1,
-                             0, st));
+        if ((rc = tf_forward(m, kv, w, tok, rows, rows_lm, L, t.logits, st))) return rc;
         DASH_HIP(launch_logprob_gather(t.logits, d.vocab, rows_lm, d.vocab, tok, Tg, L, P, d_lp + (size_t)s0 * Tg, st));
         if ((rc = dash_kv_release(kv, slots.data(), nc))) return rc;
     }
@@ -1063,6 +1101,102 @@ int dash_pg_loss(const float* d_lp, int64_t ld, int32_t T, const int32_t* d_len,
     if (T < 1 || ld < T || n_total < 1) return fail(DASH_EINVAL, "dash_pg_loss: bad sizes");
     DASH_HIP(launch_pg_loss(d_lp, ld, T, d_len, d_adv, d_kept, d_kept_count, n_total, d_loss, d_seq_lp,
                             (hipStream_t)stream));
+    return DASH_OK;
+}
+
+int dash_policy_loss(const float* d_lp, const float* d_lp_old, const float* d_kl, int64_t ld, int32_t T,
+                     const int32_t* d_len, const float* d_adv, const int32_t* d_kept, const int32_t* d_kept_count,
+                     int32_t n_total, double clip_eps, double beta, double* d_loss, double* d_stats, void* stream) {
+    if (!d_lp || !d_adv || !d_kept || !d_kept_count || !d_loss)
+        return fail(DASH_EINVAL, "dash_policy_loss: NULL argument");
+    if (T < 1 || ld < T || n_total < 1) return fail(DASH_EINVAL, "dash_policy_loss: bad sizes");
+    if (d_lp_old && !(clip_eps >= 0.0 && clip_eps < 1.0))
+        return fail(DASH_EINVAL, "dash_policy_loss: clip_eps must lie in [0, 1)");
+    if (!std::isfinite(beta)) return fail(DASH_EINVAL, "dash_policy_loss: beta must be finite");
+    DASH_HIP(launch_policy_loss(d_lp, d_lp_old, d_kl, ld, T, d_len, d_adv, d_kept, d_kept_count, n_total, clip_eps,
+                                beta, d_loss, nullptr, d_stats, (hipStream_t)stream));
+    return DASH_OK;
+}
+
+int dash_logits_kl(const float* d_theta, const float* d_base, int64_t ld, int32_t rows, int32_t vocab, float* d_kl,
+                   float* d_kl_rev, void* stream) {
+    if (!d_theta || !d_base || !d_kl) return fail(DASH_EINVAL, "dash_logits_kl: NULL argument");
+    if (rows < 0 || vocab < 1 || ld < vocab) return fail(DASH_EINVAL, "dash_logits_kl: bad sizes");
+    DASH_HIP(launch_logits_kl(d_theta, d_base, ld, rows, vocab, d_kl, d_kl_rev, (hipStream_t)stream));
+    return DASH_OK;
+}
+
+size_t dash_teacher_forced_kl_workspace_bytes(const dash_model* m, int32_t seqs_per_chunk, int32_t L, int32_t P) {
+    if (!m || seqs_per_chunk < 1 || P < 1 || L <= P) return 0;
+    return plan_tf_kl(m, seqs_per_chunk, L, P, nullptr).bytes;
+}
+
+int dash_teacher_forced_kl(dash_model* m, dash_model* base, dash_kv* kv, const int32_t* d_tokens, int32_t n_seqs,
+                           int32_t L, int32_t P, float* d_lp, float* d_kl, float* d_kl_rev, void* ws, size_t ws_bytes,
+                           void* stream) {
+    if (!m || !base || !kv || !d_tokens || !d_kl || !ws) return fail(DASH_EINVAL, "dash_teacher_forced_kl: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (!same_architecture(m->d, base->d))
+        return fail(DASH_EINVAL, "the base model must have the policy model's architecture");
+    if (n_seqs < 1 || P < 1 || L <= P) return fail(DASH_EINVAL, "need n_seqs >= 1 and 1 <= prompt_len < seq_len");
+    if (L > kv->max_ctx) return fail(DASH_ECAPACITY, "seq_len %d exceeds max_ctx %d", L, kv->max_ctx);
+    if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
+    const hipStream_t st = (hipStream_t)stream;
+    const auto& d = m->d;
+    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    const int pps = (L + ps - 1) / ps;
+    const int Tg = L - P;
+    int cmax = std::min<int>(n_seqs, kv->g.max_seqs);
+    cmax = std::min<int>(cmax, (int)(kv->free_list.size() / pps));
+    if (cmax < 1) return fail(DASH_ECAPACITY, "the pool cannot hold one sequence of %d tokens", L);
+    int lo = 0, hi = cmax;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (plan_tf_kl(m, mid, L, P, nullptr).bytes <= ws_bytes) lo = mid;
+        else hi = mid - 1;
+    }
+    const int c = lo;
+    if (c < 1)
+        return fail(DASH_ECAPACITY, "workspace too small: %zu < %zu bytes for one sequence", ws_bytes,
+                    plan_tf_kl(m, 1, L, P, nullptr).bytes);
+    for (int j = 0; j < c; ++j)
+        if (kv->npages[j] || kv->len[j]) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
+    const TfKlWs t = plan_tf_kl(m, c, L, P, (char*)ws);
+    const Ws& w = t.step;
+    std::vector<int32_t> pos, slot, gather, slots(c);
+    for (int j = 0; j < c; ++j) slots[j] = j;
+    int rc;
+    for (int s0 = 0; s0 < n_seqs; s0 += c) {
+        const int nc = std::min(c, n_seqs - s0);
+        for (int j = 0; j < nc; ++j) {
+            for (int p = 0; p < pps; ++p) kv->table[(size_t)j * mp + p] = kv_alloc_page(kv);
+            kv->npages[j] = pps;
+            kv->len[j] = L;
+        }
+        if ((rc = kv_push_rows(kv, 0, nc - 1, st))) return rc;
+        const int rows = nc * L, rows_lm = nc * Tg;
+        pos.resize(rows);
+        slot.resize(rows);
+        gather.resize(rows_lm);
+        for (int i = 0; i < rows; ++i) {
+            pos[i] = i % L;
+            slot[i] = i / L;
+        }
+        for (int i = 0; i < rows_lm; ++i) gather[i] = (i / Tg) * L + P - 1 + i % Tg;
+        if ((rc = kv_upload(kv, w.pos, pos.data(), (size_t)rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.slot, slot.data(), (size_t)rows * 4, st))) return rc;
+        if ((rc = kv_upload(kv, w.gather, gather.data(), (size_t)rows_lm * 4, st))) return rc;
+        const int32_t* tok = d_tokens + (size_t)s0 * L;
+        // the base model first: its cache entries are then overwritten by the policy's
+        if ((rc = tf_forward(base, kv, w, tok, rows, rows_lm, L, t.logits_base, st))) return rc;
+        if ((rc = tf_forward(m, kv, w, tok, rows, rows_lm, L, t.logits, st))) return rc;
+        if (d_lp)
+            DASH_HIP(launch_logprob_gather(t.logits, d.vocab, rows_lm, d.vocab, tok, Tg, L, P, d_lp + (size_t)s0 * Tg,
+                                           st));
+        DASH_HIP(launch_logits_kl(t.logits, t.logits_base, d.vocab, rows_lm, d.vocab, d_kl + (size_t)s0 * Tg,
+                                  d_kl_rev ? d_kl_rev + (size_t)s0 * Tg : nullptr, st));
+        if ((rc = dash_kv_release(kv, slots.data(), nc))) return rc;
+    }
     return DASH_OK;
 }
 

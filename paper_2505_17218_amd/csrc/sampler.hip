@@ -222,6 +222,103 @@ logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const 
     lp_out[b] = l - mx - logf(z);
 }
 
+// KL divergence between the next-token distributions of two models, one
+// workgroup per row pair, with the samplers' entry walk (groups of four, stride
+// 256 groups).  Each side keeps, over its entries of nonzero probability (logit
+// not -inf), a running maximum m, z = sum e^(x - m) and w = sum e^(x - m) (x - y)
+// with y the other side's logit: exponentials by the hardware, sums in fp64.  Then
+//   D_KL(p_x || p_y) = w_x / z_x - (m_x - m_y) - (ln z_x - ln z_y),
+// and identical rows give exactly 0 (both sides run the same operations).  An
+// entry with mass on one side and none on the other makes that direction +inf.
+struct KlAcc {
+    float m;
+    double z, w;
+    int inf;
+};
+
+DASH_DEV void kl_push(KlAcc& s, float x, float y) {
+    if (x == -INFINITY) return;
+    const bool none = y == -INFINITY;
+    const double d = none ? 0.0 : (double)x - (double)y;
+    s.inf |= none;
+    if (x > s.m) {
+        const double c = s.m == -INFINITY ? 0.0 : (double)__expf(s.m - x);
+        s.z = s.z * c + 1.0;
+        s.w = s.w * c + d;
+        s.m = x;
+    } else {  // also NaN, which then reaches z and the result
+        const double e = (double)__expf(x - s.m);
+        s.z += e;
+        s.w += e * d;
+    }
+}
+
+DASH_DEV void kl_merge(KlAcc& s, float om, double oz, double ow, int oinf) {
+    s.inf |= oinf;
+    const float m = fmaxf(s.m, om);
+    const double a = s.m == -INFINITY ? 0.0 : (double)__expf(s.m - m);
+    const double b = om == -INFINITY ? 0.0 : (double)__expf(om - m);
+    s.z = s.z * a + oz * b;
+    s.w = s.w * a + ow * b;
+    s.m = m;
+}
+
+DASH_DEV double kl_final(const KlAcc& x, const KlAcc& y) {
+    if (x.inf) return INFINITY;
+    return x.w / x.z - ((double)x.m - (double)y.m) - (log(x.z) - log(y.z));
+}
+
+__global__ void __launch_bounds__(kThreads)
+kl_rows_k(const float* __restrict__ theta, const float* __restrict__ base, int64_t ld, int vocab,
+          float* __restrict__ kl, float* __restrict__ kl_rev, int vec4) {
+    __shared__ float red_m[2][kThreads / 64];
+    __shared__ double red_z[2][kThreads / 64], red_w[2][kThreads / 64];
+    __shared__ int red_inf[2][kThreads / 64];
+    const int r = blockIdx.x;
+    const float* ra = theta + (int64_t)r * ld;
+    const float* rb = base + (int64_t)r * ld;
+    KlAcc sa{-INFINITY, 0.0, 0.0, 0}, sb{-INFINITY, 0.0, 0.0, 0};
+    const int n4 = (vocab + 3) >> 2;
+    for (int g = threadIdx.x; g < n4; g += kThreads) {
+        float a[4], b[4];
+        if (vec4 && 4 * g + 3 < vocab) {
+            const float4 va = *reinterpret_cast<const float4*>(ra + 4 * g);
+            const float4 vb = *reinterpret_cast<const float4*>(rb + 4 * g);
+            a[0] = va.x; a[1] = va.y; a[2] = va.z; a[3] = va.w;
+            b[0] = vb.x; b[1] = vb.y; b[2] = vb.z; b[3] = vb.w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {  // entries past the vocabulary have no mass on either side
+                a[j] = 4 * g + j < vocab ? ra[4 * g + j] : -INFINITY;
+                b[j] = 4 * g + j < vocab ? rb[4 * g + j] : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            kl_push(sa, a[j], b[j]);
+            kl_push(sb, b[j], a[j]);
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        kl_merge(sa, __shfl_xor(sa.m, o, 64), __shfl_xor(sa.z, o, 64), __shfl_xor(sa.w, o, 64), __shfl_xor(sa.inf, o, 64));
+        kl_merge(sb, __shfl_xor(sb.m, o, 64), __shfl_xor(sb.z, o, 64), __shfl_xor(sb.w, o, 64), __shfl_xor(sb.inf, o, 64));
+    }
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red_m[0][w] = sa.m; red_z[0][w] = sa.z; red_w[0][w] = sa.w; red_inf[0][w] = sa.inf;
+        red_m[1][w] = sb.m; red_z[1][w] = sb.z; red_w[1][w] = sb.w; red_inf[1][w] = sb.inf;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int i = 1; i < kThreads / 64; ++i) {
+        kl_merge(sa, red_m[0][i], red_z[0][i], red_w[0][i], red_inf[0][i]);
+        kl_merge(sb, red_m[1][i], red_z[1][i], red_w[1][i], red_inf[1][i]);
+    }
+    kl[r] = (float)kl_final(sb, sa);  // D_KL(p_base || p_theta)
+    if (kl_rev) kl_rev[r] = (float)kl_final(sa, sb);
+}
+
 }  // namespace
 
 hipError_t launch_logprob_gather(const float* logits, int64_t ld, int rows, int vocab, const int32_t* tokens, int per,
@@ -230,6 +327,16 @@ hipError_t launch_logprob_gather(const float* logits, int64_t ld, int rows, int 
     if (per < 1) return hipErrorInvalidValue;
     const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
     logprob_gather_k<<<rows, kThreads, 0, st>>>(logits, ld, vocab, tokens, per, stride, off, lp_out, vec4);
+    return hipGetLastError();
+}
+
+hipError_t launch_logits_kl(const float* theta, const float* base, int64_t ld, int rows, int vocab, float* kl,
+                            float* kl_rev, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    if (vocab < 1 || ld < vocab) return hipErrorInvalidValue;
+    const int vec4 =
+        ((ld & 3) == 0 && ((uintptr_t)theta & 15) == 0 && ((uintptr_t)base & 15) == 0) ? 1 : 0;
+    kl_rows_k<<<rows, kThreads, 0, st>>>(theta, base, ld, vocab, kl, kl_rev, vec4);
     return hipGetLastError();
 }
 

@@ -198,6 +198,56 @@ def pg_loss(logprobs: torch.Tensor, adv: torch.Tensor, kept: torch.Tensor, lengt
     return loss, seq
 
 
+def policy_loss(logprobs: torch.Tensor, adv: torch.Tensor, kept: torch.Tensor, lengths: torch.Tensor | None = None,
+                logprobs_old: torch.Tensor | None = None, kl: torch.Tensor | None = None, clip_eps: float = 0.2,
+                beta: float = 0.0):
+    """dash_policy_loss: (float64 loss [1], float64 stats [N, 4] = (S, S_old, KL, d loss / d S) per kept sample)."""
+    N, T = logprobs.shape
+    dev = logprobs.device
+    for t in (logprobs_old, kl):
+        if t is not None and (t.shape != logprobs.shape or t.stride() != logprobs.stride()):
+            raise ValueError("logprobs_old and kl must have the logprobs' shape and strides")
+    cnt = torch.tensor([kept.numel()], dtype=torch.int32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stats = torch.zeros(N, 4, dtype=torch.float64, device=dev)
+    kept_buf = kept if kept.numel() else torch.zeros(1, dtype=torch.int32, device=dev)
+    L.dash_policy_loss(logprobs.data_ptr(), logprobs_old.data_ptr() if logprobs_old is not None else None,
+                       kl.data_ptr() if kl is not None else None, logprobs.stride(0), T,
+                       lengths.data_ptr() if lengths is not None else None, adv.data_ptr(), kept_buf.data_ptr(),
+                       cnt.data_ptr(), N, clip_eps, beta, loss.data_ptr(), stats.data_ptr(), stream_handle())
+    return loss, stats
+
+
+def logits_kl(theta: torch.Tensor, base: torch.Tensor, reverse: bool = True):
+    """dash_logits_kl on float32 [rows, V] logits: (D_KL(base || theta) [rows], D_KL(theta || base) [rows] or None)."""
+    if theta.shape != base.shape or theta.stride() != base.stride() or theta.dim() != 2:
+        raise ValueError("theta and base logits must be 2-D with equal shapes and strides")
+    rows, V = theta.shape
+    kl = torch.empty(rows, dtype=torch.float32, device=theta.device)
+    kl_rev = torch.empty(rows, dtype=torch.float32, device=theta.device) if reverse else None
+    L.dash_logits_kl(theta.data_ptr(), base.data_ptr(), theta.stride(0), rows, V, kl.data_ptr(),
+                     kl_rev.data_ptr() if kl_rev is not None else None, stream_handle())
+    return kl, kl_rev
+
+
+def teacher_forced_kl(model: Model, base: Model, kv: KVCache, seqs: torch.Tensor, prompt_len: int,
+                      seqs_per_chunk: int = 8, with_logprobs: bool = True, reverse: bool = True):
+    """dash_teacher_forced_kl: int32 [n, L] -> (log-probs or None, KL(base || policy), KL(policy || base) or None),
+    each float32 [n, L - prompt_len]."""
+    n, Ls = seqs.shape
+    shp = (n, Ls - prompt_len)
+    lp = torch.empty(shp, dtype=torch.float32, device=seqs.device) if with_logprobs else None
+    kl = torch.empty(shp, dtype=torch.float32, device=seqs.device)
+    kl_rev = torch.empty(shp, dtype=torch.float32, device=seqs.device) if reverse else None
+    c = max(1, min(seqs_per_chunk, n))
+    nbytes = L.dash_teacher_forced_kl_workspace_bytes(model.handle, c, Ls, prompt_len)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=seqs.device)
+    L.dash_teacher_forced_kl(model.handle, base.handle, kv.handle, seqs.data_ptr(), n, Ls, prompt_len,
+                             lp.data_ptr() if lp is not None else None, kl.data_ptr(),
+                             kl_rev.data_ptr() if kl_rev is not None else None, aligned(ws), nbytes, stream_handle())
+    return lp, kl, kl_rev
+
+
 class Rollout:
     """Reusable buffers for dash_rollout on one workload shape."""
 

@@ -141,6 +141,37 @@ def test_recompute_loss_and_profiler_validation():
     assert e.value.status == L.DASH_EINVAL
 
 
+def test_kl_and_policy_loss_validation():
+    d = _desc()
+    h = L.dash_model_create(d, _fake_ptrs(d))
+    # the teacher-forced KL keeps two logits buffers per chunk
+    w1 = L.dash_teacher_forced_kl_workspace_bytes(h, 1, 48, 16)
+    assert w1 >= L.dash_teacher_forced_workspace_bytes(h, 1, 48, 16) + 32 * d.vocab * 4
+    assert L.dash_teacher_forced_kl_workspace_bytes(h, 1, 16, 16) == 0
+    assert L.dash_teacher_forced_kl_workspace_bytes(h, 0, 48, 16) == 0
+    for base, kv in [(None, 0x100), (h, None)]:
+        with pytest.raises(L.DashError) as e:  # NULL base / kv handle
+            L.dash_teacher_forced_kl(h, base, kv, 0x1000, 2, 48, 16, None, 0x2000, None, 0x3000, w1, None)
+        assert e.value.status == L.DASH_EINVAL
+    L.dash_model_destroy(h)
+    for args in [(None, 0x2000, 8, 4, 8),    # no theta logits
+                 (0x1000, 0x2000, 4, 4, 8),  # ld < vocab
+                 (0x1000, 0x2000, 8, 4, 0),  # empty vocabulary
+                 (0x1000, 0x2000, 8, -1, 8)]:  # negative row count
+        with pytest.raises(L.DashError) as e:
+            L.dash_logits_kl(args[0], args[1], args[2], args[3], args[4], 0x3000, None, None)
+        assert e.value.status == L.DASH_EINVAL
+    base = (0x1000, 0x1100, 0x1200, 8, 8, None, 0x2000, 0x3000, 0x4000, 4)
+    for change, eps, beta in [({0: None}, 0.2, 0.0), ({3: 4}, 0.2, 0.0), ({9: 0}, 0.2, 0.0),
+                              ({}, 1.0, 0.0), ({}, -0.1, 0.0), ({}, float("nan"), 0.0), ({}, 0.2, float("inf"))]:
+        a = list(base)
+        for i, v in change.items():
+            a[i] = v
+        with pytest.raises(L.DashError) as e:
+            L.dash_policy_loss(*a, eps, beta, 0x5000, None, None)
+        assert e.value.status == L.DASH_EINVAL
+
+
 def test_kv_sizes():
     d = _desc()
     h = L.dash_model_create(d, _fake_ptrs(d))
