@@ -33,6 +33,12 @@ constexpr float kScreenTol = 1.6e-5f;
 
 DASH_DEV bool better(float s, int i, float bs, int bi) { return s > bs || (s == bs && i < bi); }
 
+// Non-temporal (streaming) vector load, for logits read once.
+DASH_DEV float4 load_stream4(const float* p) {
+    const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // -ln(-ln u) with the hardware logarithm; u = ((x >> 8) | 1) 2^-24 as in gumbel_from_bits
 DASH_DEV float cheap_gumbel(uint32_t x) {
     const float u = (float)((x >> 8) | 1u) * (1.0f / 16777216.0f);
@@ -282,8 +288,8 @@ kl_rows_k(const float* __restrict__ theta, const float* __restrict__ base, int64
     for (int g = threadIdx.x; g < n4; g += kThreads) {
         float a[4], b[4];
         if (vec4 && 4 * g + 3 < vocab) {
-            const float4 va = *reinterpret_cast<const float4*>(ra + 4 * g);
-            const float4 vb = *reinterpret_cast<const float4*>(rb + 4 * g);
+            const float4 va = load_stream4(ra + 4 * g);
+            const float4 vb = load_stream4(rb + 4 * g);
             a[0] = va.x; a[1] = va.y; a[2] = va.z; a[3] = va.w;
             b[0] = vb.x; b[1] = vb.y; b[2] = vb.z; b[3] = vb.w;
         } else {
