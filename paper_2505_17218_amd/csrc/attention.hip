@@ -31,11 +31,13 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferDword3 = 0x00020000;
-// Cache policy of the K/V block loads: non-temporal (streaming).  Every KV byte is
-// read once per step (the rows of a prompt group share prompt pages while they run
-// together); measured on gfx950 with the last-level cache cold, the plain policy
-// streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.
-constexpr int kKvLoadPolicy = 2;
+// Cache policies of the K/V block loads.  Decode streams (non-temporal): every KV
+// byte is read once per step (the rows of a prompt group share prompt pages while
+// they run together); measured on gfx950 with the last-level cache cold, the plain
+// policy streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.
+// Prefill keeps the default: each key block is read again by every 16-query column
+// block of its sequence and should stay cached (streaming it measured 1.75x slower).
+constexpr int kKvStream = 2, kKvReuse = 0;
 constexpr int kMaxGroupWaves = 16;  // samples per group served by one workgroup  // raw buffer resource word 3 (gfx9 family): out-of-range reads give 0
 
 // ---- shared MFMA block step ---------------------------------------------
@@ -52,7 +54,7 @@ struct KVRegs {
 // Buffer loads over the page's K and V blocks: an unbacked page gets an empty
 // range and reads as zeros, so the loads carry no branch and the next block can
 // be in flight while the current one is multiplied.
-template <int HD>
+template <int HD, int POLICY>
 DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps, int kin, bool ok, int col, int grp) {
     const int bytes = ok ? ps * HD * 2 : 0;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(kb), 0, bytes, kBufferDword3);
@@ -63,11 +65,11 @@ DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps,
         for (int c = 0; c < HD / 32; ++c)
             r.k[h][c] = __builtin_bit_cast(
                 uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (((c * ps + kin + h * 16 + col) * 32 + grp * 8) * 2), 0,
-                                                             kKvLoadPolicy));
+                                                             POLICY));
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d)
         r.v[d] = __builtin_bit_cast(
-            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((d * 16 + col) * ps + kin + grp * 8) * 2, 0, kKvLoadPolicy));
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((d * 16 + col) * ps + kin + grp * 8) * 2, 0, POLICY));
 }
 
 template <int HD>
@@ -216,8 +218,8 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
-                    key0 % g.page_size, ok, head, grp);
+        load_kv<HD, kKvStream>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1),
+                               g.page_size, key0 % g.page_size, ok, head, grp);
     };
     fetch(r[0], b_begin);
     for (int b = b_begin; b < b_end; b += 2) {
@@ -371,8 +373,9 @@ decode_attn_group_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict
                 int page = kv_page_of(g, page_table, sl, key0);
                 const bool ok = page >= 0;
                 page = ok ? page : 0;
-                load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1),
-                            g.page_size, key0 % g.page_size, ok, head, grp);
+                load_kv<HD, kKvStream>(dst, pool + kv_block(g, layer, page, kvh, 0),
+                                       pool + kv_block(g, layer, page, kvh, 1), g.page_size, key0 % g.page_size, ok,
+                                       head, grp);
             };
             fetch(r[0], bp0);
             for (int b = bp0; b < b_end; b += 2) {
@@ -439,8 +442,8 @@ __global__ void __launch_bounds__(64) prefill_attn_bf16_k(const bf16_t* __restri
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        load_kv<HD>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1), g.page_size,
-                    key0 % g.page_size, ok, col, grp);
+        load_kv<HD, kKvReuse>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1),
+                              g.page_size, key0 % g.page_size, ok, col, grp);
     };
     fetch(r[0], 0);
     for (int b = 0; b < nblk; b += 2) {
