@@ -5,10 +5,11 @@
 // v_mfma_f32_16x16x32_bf16:
 //   S^T[key, head] = K[key, :] . Q[head, :]      (A = K tile, B = Q^T)
 //   O^T[dim, head] += V^T[dim, key] . P^T[key, head]   (A = V^T tile, B = P^T)
-// The K page layout ([chunk of 32 dims][key][32]) and the transposed,
-// key-permuted V page layout make every A-operand load a 16-byte read per lane
-// and a contiguous 1 KB per wave, straight from HBM into VGPRs: nothing is
-// shared between waves, so there is no LDS round trip.  The S^T accumulator
+// The K page layout ([chunk of 32 dims][key][32]) and the transposed V page
+// layout (dim-major groups of 8 keys, see v_index_bf16) make every A-operand load
+// a 16-byte read per lane (K: a contiguous 1 KB per wave; V: four 256-byte runs),
+// straight from HBM into VGPRs: nothing is shared between waves, so there is no
+// LDS round trip.  The S^T accumulator
 // gives each lane 4 consecutive keys of one head per 16-key half; those 8
 // probabilities are exactly the lane's P^T operand, so no shuffles are needed
 // between the two MFMAs.  Online softmax in fp32 (base 2), with per-lane partial
@@ -69,7 +70,8 @@ DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps,
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d)
         r.v[d] = __builtin_bit_cast(
-            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((d * 16 + col) * ps + kin + grp * 8) * 2, 0, POLICY));
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((((kin >> 5) * 4 + grp) * HD + d * 16 + col) * 8) * 2, 0,
+                                                         POLICY));
 }
 
 template <int HD>
@@ -328,7 +330,7 @@ decode_attn_group_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict
             const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
                 const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, 1)), 0, bytes, kBufferDword3);
             return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                rv, ((d * 16 + head) * g.page_size + kin + grp * 8) * 2, 0, 0));
+                rv, ((((kin >> 5) * 4 + grp) * HD + d * 16 + head) * 8) * 2, 0, 0));
         };
         constexpr int FPW = (NF + NW - 1) / NW;  // fragments per wave
         uint4 stage[FPW];

@@ -108,15 +108,20 @@ DASH_DEV size_t kv_block(const KVGeom& g, int layer, int page, int kvh, int kind
     return ((((size_t)layer * g.n_pages + page) * g.n_kv + kvh) * 2 + kind) * (size_t)g.page_size * g.head_dim;
 }
 
-DASH_DEV int vperm32(int k) { return 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3); }
 
 // Element index inside a block.
 DASH_DEV size_t k_index_f32(const KVGeom& g, int key, int d) { return (size_t)key * g.head_dim + d; }
 DASH_DEV size_t k_index_bf16(const KVGeom& g, int key, int d) {
     return ((size_t)(d >> 5) * g.page_size + key) * 32 + (d & 31);
 }
+// bf16 V block: [ps / 32][4][hd][8].  Each run of 32 keys is split into four
+// groups of 8 (group j: keys 4j .. 4j+3 and 16+4j .. 16+4j+3, the keys whose scores
+// one lane of the score MFMA holds), stored dim-major with the group's 8 keys
+// contiguous: a lane's P.V operand is one 16-byte read, and appending one key
+// writes 16-byte-strided values (32 lines of 64 bytes per kv head at hd = 128).
 DASH_DEV size_t v_index_bf16(const KVGeom& g, int key, int d) {
-    return (size_t)d * g.page_size + (key & ~31) + vperm32(key & 31);
+    const int kk = key & 31, grp = (kk & 15) >> 2, p = (kk & 3) + ((kk >> 4) << 2);
+    return ((size_t)((key >> 5) * 4 + grp) * g.head_dim + d) * 8 + p;
 }
 
 template <typename T> DASH_DEV size_t k_index(const KVGeom& g, int key, int d);

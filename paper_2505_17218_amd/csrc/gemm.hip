@@ -153,6 +153,52 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
         }
     };
 
+    // QKV epilogue inputs, fetched before the main loop so that their latency (for the
+    // k / v tiles a dependent chain: position and slot, then the page table) hides
+    // behind it: per tile row its cache page (or -1) and key within the page; per
+    // thread the bias and the RoPE cosines / sines of its pairs.
+    [[maybe_unused]] __shared__ int row_page[EPI == EPI_QKV_ROPE ? BM : 1], row_key[EPI == EPI_QKV_ROPE ? BM : 1];
+    constexpr int kRows = EPI == EPI_QKV_ROPE ? BM * (BN / 2) / NT : 1;   // RoPE pairs per thread
+    constexpr int kRowsV = EPI == EPI_QKV_ROPE ? BM * BN / NT : 1;        // v elements per thread
+    [[maybe_unused]] float2 rope_cs[kRows];
+    [[maybe_unused]] float bias_a = 0.f, bias_b = 0.f;
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        static_assert(BM * (BN / 2) % NT == 0 && NT % (BN / 2) == 0, "RoPE pair mapping");
+        static_assert(BM * BN % NT == 0 && NT % BN == 0, "v mapping");
+        const KVGeom& g = qa.g;
+        const int hd = g.head_dim, half = hd >> 1;
+        const int lg_half = hd == 128 ? 6 : 5;  // head_dim is 64 or 128
+        const int n0 = nt * BN;
+        const int q_cols = qa.n_heads * hd, k_end_col = q_cols + g.n_kv * hd;
+        if (n0 >= q_cols && tid < BM) {
+            const int m = m0 + tid;
+            int page = -1, key = 0;
+            if (m < M) {
+                const int p = qa.pos[m];
+                page = kv_page_of(g, qa.page_table, qa.slot[m], p);
+                key = p % g.page_size;
+                if (page < 0 && n0 < k_end_col && qa.status) atomicOr(qa.status, 1u);
+            }
+            row_page[tid] = page;
+            row_key[tid] = key;
+        }
+        if (n0 < k_end_col) {  // q / k tile: thread t takes pair t % (BN/2) of rows t / (BN/2) + u NT / (BN/2)
+            const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
+            const int hl = pi >> lg_half, i = pi & (half - 1);
+            const int n = n0 + hl * hd + i;
+            bias_a = bf2f(qa.bias[n]);
+            bias_b = bf2f(qa.bias[n + half]);
+#pragma unroll
+            for (int u = 0; u < kRows; ++u) {
+                const int m = min(m0 + r0 + u * (NT / (BN / 2)), M - 1);
+                rope_cs[u] = *reinterpret_cast<const float2*>(qa.cs + ((size_t)m * half + i) * 2);
+            }
+        } else {  // v tile: thread t takes column t % BN of rows t / BN + u NT / BN
+            const int n = n0 + tid % BN;
+            bias_a = n < N ? bf2f(qa.bias[n]) : 0.f;
+        }
+    }
+
     const int n_k = (k_end - k_begin + kBK - 1) / kBK;
 #pragma unroll
     for (int p = 0; p < PD; ++p) load(p, k_begin + p * kBK);
@@ -188,37 +234,21 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
         __syncthreads();
         const KVGeom& g = qa.g;
         const int hd = g.head_dim, half = hd >> 1;
-        const int lg_half = hd == 128 ? 6 : 5;  // head_dim is 64 or 128
+        const int lg_half = hd == 128 ? 6 : 5;
         const int n0 = nt * BN;
         const int q_cols = qa.n_heads * hd, k_end = q_cols + g.n_kv * hd;
-        // per row of the tile: its cache page (or -1) and key within the page, looked up once
-        __shared__ int row_page[BM], row_key[BM];
-        if (n0 >= q_cols && tid < BM) {
-            const int m = m0 + tid;
-            int page = -1, key = 0;
-            if (m < M) {
-                const int p = qa.pos[m];
-                page = kv_page_of(g, qa.page_table, qa.slot[m], p);
-                key = p % g.page_size;
-                if (page < 0 && n0 < k_end && qa.status) atomicOr(qa.status, 1u);
-            }
-            row_page[tid] = page;
-            row_key[tid] = key;
-        }
-        __syncthreads();
         if (n0 < k_end) {
-            // one thread per RoPE pair; consecutive threads take consecutive dims of one row
-            for (int it = tid; it < BM * (BN / 2); it += NT) {
-                const int rl = it / (BN / 2), pi = it - rl * (BN / 2);
-                const int m = m0 + rl;
+            const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
+            const int hl = pi >> lg_half, i = pi & (half - 1);
+            const int c = hl * hd + i, n = n0 + c;
+#pragma unroll
+            for (int u = 0; u < kRows; ++u) {
+                const int rl = r0 + u * (NT / (BN / 2)), m = m0 + rl;
                 if (m >= M) continue;
-                const int hl = pi >> lg_half, i = pi & (half - 1);
-                const int c = hl * hd + i, n = n0 + c;
-                const float a = Cs[rl * CS + c] + bf2f(qa.bias[n]);
-                const float b = Cs[rl * CS + c + half] + bf2f(qa.bias[n + half]);
-                const float2 cs = *reinterpret_cast<const float2*>(qa.cs + ((size_t)m * half + i) * 2);
+                const float a = Cs[rl * CS + c] + bias_a;
+                const float b = Cs[rl * CS + c + half] + bias_b;
                 float lo, hi;
-                rope_pair(a, b, cs.x, cs.y, lo, hi);
+                rope_pair(a, b, rope_cs[u].x, rope_cs[u].y, lo, hi);
                 if (n < q_cols) {
                     bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + n / hd) * hd;
                     q[i] = f2bf(lo);
@@ -230,12 +260,13 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
                 }
             }
         } else {
-            for (int it = tid; it < BM * BN; it += NT) {
-                const int rl = it / BN, c = it - rl * BN;
-                const int m = m0 + rl, n = n0 + c;
+            const int c = tid % BN, r0 = tid / BN;
+            const int n = n0 + c, jj = n - k_end;
+#pragma unroll
+            for (int u = 0; u < kRowsV; ++u) {
+                const int rl = r0 + u * (NT / BN), m = m0 + rl;
                 if (m >= M || n >= N || row_page[rl] < 0) continue;
-                const float v = Cs[rl * CS + c] + bf2f(qa.bias[n]);
-                const int jj = n - k_end;
+                const float v = Cs[rl * CS + c] + bias_a;
                 bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
                 vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))] = f2bf(v);
             }
