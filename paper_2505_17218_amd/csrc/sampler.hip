@@ -54,6 +54,22 @@ DASH_DEV float wave_max_f(float v) {
     return v;
 }
 
+// Entries 4g .. 4g+3 of a row (NaN past the vocabulary or for g >= n4): one 16-byte
+// load when the row allows it.
+DASH_DEV void fetch4(const float* row, int g, int n4, int vocab, int vec4, float (&l)[4]) {
+    if (g < n4 && vec4 && 4 * g + 3 < vocab) {
+        const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
+        l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) l[j] = (g < n4 && 4 * g + j < vocab) ? row[4 * g + j] : NAN;
+    }
+}
+
+// UNIT_T: temperature 1, no division (a runtime select would still evaluate the
+// exact division for every entry).  The next iteration's entries are loaded before
+// the current ones are scored, so their latency overlaps the arithmetic.
+template <bool UNIT_T>
 __global__ void __launch_bounds__(kThreads)
 sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ row_of,
          const int32_t* __restrict__ uid, const int32_t* __restrict__ step, float temperature, uint32_t k0,
@@ -67,7 +83,6 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     const int r = row_of ? row_of[b] : b;
     const float* row = logits + (int64_t)r * ld;
     const uint32_t u_id = (uint32_t)uid[b], st = (uint32_t)step[b];
-    const bool unit_t = temperature == 1.0f;
 
     float best_s = -INFINITY;
     int best_i = 0x7FFFFFFF;
@@ -76,24 +91,20 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     const int n4 = (vocab + 3) >> 2;
     // every lane of the wave runs the same number of iterations (the shared bound needs all lanes)
     const int lane0 = threadIdx.x & ~63;
+    float nxt[4];
+    fetch4(row, lane0 + (threadIdx.x & 63), n4, vocab, vec4, nxt);
     for (int g0 = lane0; g0 < n4; g0 += kThreads) {
         const int g = g0 + (threadIdx.x & 63);
+        float l[4] = {nxt[0], nxt[1], nxt[2], nxt[3]};
+        fetch4(row, g + kThreads, n4, vocab, vec4, nxt);
         float floor_t = floor_w;
         if (g < n4) {
-            float l[4];
-            if (vec4 && 4 * g + 3 < vocab) {
-                const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
-                l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
-            }
             const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, k0, k1);
             const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (!isfinite(l[j])) continue;
-                const float sc = unit_t ? l[j] : div_rn(l[j], temperature);
+                const float sc = UNIT_T ? l[j] : div_rn(l[j], temperature);
                 const float sa = sc + cheap_gumbel(xs[j]);
                 const float mg = screen_margin(sa);
                 if (sa + mg >= floor_t) {
@@ -152,7 +163,7 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     float lp = NAN;
     if (best_i != 0x7FFFFFFF) {
         tok = best_i;
-        const float sc = unit_t ? row[tok] : div_rn(row[tok], temperature);
+        const float sc = UNIT_T ? row[tok] : div_rn(row[tok], temperature);
         lp = sc - mx - logf(z);
     }
     tok_out[b] = tok;
@@ -184,15 +195,11 @@ logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const 
     const float* row = logits + (int64_t)b * ld;
     float mx = -INFINITY, z = 0.f;
     const int n4 = (vocab + 3) >> 2;
+    float nxt[4];
+    fetch4(row, threadIdx.x, n4, vocab, vec4, nxt);
     for (int g = threadIdx.x; g < n4; g += kThreads) {
-        float l[4];
-        if (vec4 && 4 * g + 3 < vocab) {
-            const float4 v = *reinterpret_cast<const float4*>(row + 4 * g);
-            l[0] = v.x; l[1] = v.y; l[2] = v.z; l[3] = v.w;
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) l[j] = 4 * g + j < vocab ? row[4 * g + j] : NAN;
-        }
+        float l[4] = {nxt[0], nxt[1], nxt[2], nxt[3]};
+        fetch4(row, g + kThreads, n4, vocab, vec4, nxt);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (!isfinite(l[j])) continue;
@@ -359,8 +366,12 @@ hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, c
                          hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
-    sample_k<<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
-                                        (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
+    if (temperature == 1.0f)
+        sample_k<true><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
+                                                  (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
+    else
+        sample_k<false><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
+                                                   (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
     return hipGetLastError();
 }
 
