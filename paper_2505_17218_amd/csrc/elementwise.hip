@@ -91,12 +91,13 @@ __global__ void __launch_bounds__(kRowThreads) add_rmsnorm_k(float* __restrict__
     const int i_out = blockIdx.x;
     const int r = row_map ? row_map[i_out] : i_out;
     const int d4 = d >> 2;
-    float4 v[kMaxV];
+    float4 v[kMaxV], wt[kMaxV];
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxV; ++j) {
         const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
+            wt[j] = load4(w + 4 * i);  // the norm weights too, so no load waits after the reduction
             // all loads of this float4 are issued before the first add
             float4 p[kMaxSplits];
 #pragma unroll
@@ -120,7 +121,7 @@ __global__ void __launch_bounds__(kRowThreads) add_rmsnorm_k(float* __restrict__
         const int i = threadIdx.x + kRowThreads * j;
         if (i < d4) {
             if (write_x) *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = v[j];
-            const float4 g = load4(w + 4 * i);
+            const float4 g = wt[j];
             store4(y + (size_t)i_out * d + 4 * i, make_float4(v[j].x * inv * g.x, v[j].y * inv * g.y,
                                                               v[j].z * inv * g.z, v[j].w * inv * g.w));
         }
