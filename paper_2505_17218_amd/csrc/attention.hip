@@ -32,10 +32,11 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferDword3 = 0x00020000;
-// Cache policies of the K/V block loads.  Decode streams (non-temporal): every KV
-// byte is read once per step (the rows of a prompt group share prompt pages while
-// they run together); measured on gfx950 with the last-level cache cold, the plain
-// policy streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.
+// Cache policies of the K/V block loads.  Decode streams (non-temporal) the blocks
+// that only one row reads: measured on gfx950 with the last-level cache cold, the
+// plain policy streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.
+// Blocks below KVGeom::shared_keys (a prompt group's shared pages, read by all the
+// group's rows at about the same time) keep the default policy.
 // Prefill keeps the default: each key block is read again by every 16-query column
 // block of its sequence and should stay cached (streaming it measured 1.75x slower).
 constexpr int kKvStream = 2, kKvReuse = 0;
@@ -220,8 +221,12 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
         int page = kv_page_of(g, page_table, sl, key0);
         const bool ok = page >= 0;
         page = ok ? page : 0;
-        load_kv<HD, kKvStream>(dst, pool + kv_block(g, layer, page, kvh, 0), pool + kv_block(g, layer, page, kvh, 1),
-                               g.page_size, key0 % g.page_size, ok, head, grp);
+        const bf16_t* kb = pool + kv_block(g, layer, page, kvh, 0);
+        const bf16_t* vb = pool + kv_block(g, layer, page, kvh, 1);
+        if (key0 < g.shared_keys)  // wave-uniform: a prompt page the other rows of the group read too
+            load_kv<HD, kKvReuse>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
+        else
+            load_kv<HD, kKvStream>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
     };
     fetch(r[0], b_begin);
     for (int b = b_begin; b < b_end; b += 2) {

@@ -93,6 +93,8 @@ struct KVGeom {
     int max_pages;  // page-table row length (pages per slot)
     int max_seqs;   // page-table rows (slots)
     int split_keys; // decode attention context split (multiple of 32, fixed per cache)
+    int shared_keys; // positions below this are shared by several rows (a prompt group's full
+                     // pages): decode attention keeps them cached, the rest it streams
 };
 
 // Page backing position `pos` of `slot`, or -1 if the slot, position or table entry is out of range.

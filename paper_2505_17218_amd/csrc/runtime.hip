@@ -426,7 +426,7 @@ int dash_kv_create(const dash_model* m, void* pool, size_t pool_bytes, int32_t p
     kv->max_ctx = max_ctx;
     const int max_pages = (max_ctx + ps - 1) / ps;
     kv->g = KVGeom{m->d.n_layers, (int)pages, m->d.n_kv_heads, m->d.head_dim, ps, max_pages, max_seqs,
-                   attention_split_keys(max_seqs, m->d.n_kv_heads, max_ctx)};
+                   attention_split_keys(max_seqs, m->d.n_kv_heads, max_ctx), 0};
     const size_t ent = table_entries(max_seqs, max_ctx, ps);
     kv->d_table = (int32_t*)d_table;
     kv->d_status = (uint32_t*)((char*)d_table + align_up(ent * 4, 256));
@@ -1240,6 +1240,14 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     const int V = d.vocab;
     const bool ragged = std::any_of(budget.begin(), budget.end(), [&](int b) { return b != T; });
     const size_t step_ws_bytes = rw.step.bytes;
+    // the prompt's full pages are shared by the group's G rows for the whole rollout
+    // (decode attention keeps them cached); restored on every way out
+    struct SharedKeys {
+        KVGeom& g;
+        int saved;
+        ~SharedKeys() { g.shared_keys = saved; }
+    } shared_keys_scope{kv->g, kv->g.shared_keys};
+    kv->g.shared_keys = G > 1 ? P / kv->g.page_size * kv->g.page_size : 0;
 
     DASH_HIP(launch_fill_i32(d_out_tokens, -1, (size_t)N * T, st));
     int rc;
