@@ -72,3 +72,19 @@ def run_stepwise(model: engine.Model, kv: engine.KVCache, prompts: np.ndarray, g
 def make_kv(model: engine.Model, page_size: int, max_seqs: int, max_ctx: int, extra_pages: int = 8):
     pages_per_seq = (max_ctx + page_size - 1) // page_size
     return engine.KVCache(model, page_size, max_seqs, max_ctx, max_seqs * pages_per_seq + extra_pages)
+
+
+def kl_sensitivity(la: np.ndarray, lb: np.ndarray):
+    """First-order bounds of |d KL| per unit max-norm change of the logits, per row, for
+    D_KL(b || a): sum |p_a - p_b| (through a) + E_b |log(p_b / p_a) - KL| (through b);
+    and the reverse direction with the roles swapped.  A GPU KL computed from logits within
+    delta of the float64 ones lies within about delta times this of the exact KL."""
+    la = np.asarray(la, dtype=np.float64)
+    lb = np.asarray(lb, dtype=np.float64)
+    lsa = la - (la.max(1, keepdims=True) + np.log(np.exp(la - la.max(1, keepdims=True)).sum(1, keepdims=True)))
+    lsb = lb - (lb.max(1, keepdims=True) + np.log(np.exp(lb - lb.max(1, keepdims=True)).sum(1, keepdims=True)))
+    pa, pb = np.exp(lsa), np.exp(lsb)
+    kl = np.sum(pb * (lsb - lsa), 1)
+    kl_rev = np.sum(pa * (lsa - lsb), 1)
+    tv2 = np.abs(pa - pb).sum(1)
+    return tv2 + np.sum(pb * np.abs(lsb - lsa - kl[:, None]), 1), tv2 + np.sum(pa * np.abs(lsa - lsb - kl_rev[:, None]), 1)

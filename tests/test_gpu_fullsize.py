@@ -7,10 +7,11 @@ import pytest
 import torch
 
 from oracle import model as om
+from oracle import policy as opol
 from oracle import sampler as osm
 from paper_2505_17218_amd import engine, synth
 
-from gpu_util import require_gpu, shape_dict
+from gpu_util import dev_i32, kl_sensitivity, require_gpu, shape_dict
 
 pytestmark = pytest.mark.gpu
 
@@ -121,3 +122,30 @@ def test_other_workloads_sampled_against_oracle(workload, ns, ts):
             g = osm.noise(seed, n, int(t), s.vocab).astype(np.float64)
             sc = l64 + g
             assert sc[tok] >= sc.max() - 2 * LOGIT_TOL, (workload, n, t)
+
+
+def test_fullsize_teacher_forced_kl(rollout_1p5b):
+    """KL(base || policy) and its reverse along a sampled 1.5B-shape sequence (V = 151,936)
+    against an independently initialised base model of the same shape: sampled positions
+    against the oracle, within the first-order effect of the bf16 logits tolerance (twice the
+    bound plus 4 delta^2); the policy's log-probs equal the ones recorded while sampling."""
+    r = rollout_1p5b
+    wl = r["wl"]
+    s, P, n, T = wl.shape, wl.prompt_len, 13, 40
+    base_w = synth.make_weights(s, 1)
+    base = engine.Model(s, base_w)
+    seq = np.concatenate([r["prompts"][n // wl.group], r["toks"][n][:T]]).astype(np.int32)
+    lp, kl, kl_rev = engine.teacher_forced_kl(r["model"], base, r["kv"], dev_i32(seq[None, :]), P)
+    lp, kl, kl_rev = lp.cpu().numpy()[0], kl.cpu().numpy()[0], kl_rev.cpu().numpy()[0]
+    np.testing.assert_array_equal(lp.view(np.uint32), r["lps"][n, :T].view(np.uint32))
+    ts = np.array([0, 1, 17, T - 1])
+    sd = shape_dict(s)
+    la = om.forward(sd, r["weights"], seq[:P + ts.max()], positions=P - 1 + ts)
+    lb = om.forward(sd, base_w, seq[:P + ts.max()], positions=P - 1 + ts)
+    want, want_rev = opol.kl_rows(la, lb)
+    sens, sens_rev = kl_sensitivity(la, lb)
+    tol = 2 * LOGIT_TOL * sens + 4 * LOGIT_TOL ** 2
+    tol_rev = 2 * LOGIT_TOL * sens_rev + 4 * LOGIT_TOL ** 2
+    assert np.all(np.abs(kl[ts] - want) <= tol), (kl[ts], want, tol)
+    assert np.all(np.abs(kl_rev[ts] - want_rev) <= tol_rev), (kl_rev[ts], want_rev, tol_rev)
+    assert np.all(kl > 0) and np.all(np.isfinite(kl))

@@ -10,7 +10,7 @@ from oracle import policy as opol
 from paper_2505_17218_amd import _lib as L
 from paper_2505_17218_amd import engine, synth
 
-from gpu_util import dev_i32, make_kv, require_gpu, shape_dict
+from gpu_util import dev_i32, kl_sensitivity, make_kv, require_gpu, shape_dict
 
 pytestmark = pytest.mark.gpu
 
@@ -97,21 +97,6 @@ def test_logits_kl_strided_masked_and_close_rows():
             assert ref < 1e-3  # the close rows really probe small divergences
 
 
-def _kl_sensitivity(la, lb):
-    """First-order bounds of |d KL| per unit max-norm change of the logits, per row:
-    D_KL(b || a): sum |p_a - p_b| (through a) + E_b |log(p_b / p_a) - KL| (through b);
-    the reverse direction with the roles swapped."""
-    lsa = la - (la.max(1, keepdims=True) + np.log(np.exp(la - la.max(1, keepdims=True)).sum(1, keepdims=True)))
-    lsb = lb - (lb.max(1, keepdims=True) + np.log(np.exp(lb - lb.max(1, keepdims=True)).sum(1, keepdims=True)))
-    pa, pb = np.exp(lsa), np.exp(lsb)
-    kl = np.sum(pb * (lsb - lsa), 1)
-    kl_rev = np.sum(pa * (lsa - lsb), 1)
-    tv2 = np.abs(pa - pb).sum(1)
-    s = tv2 + np.sum(pb * np.abs(lsb - lsa - kl[:, None]), 1)
-    s_rev = tv2 + np.sum(pa * np.abs(lsa - lsb - kl_rev[:, None]), 1)
-    return s, s_rev
-
-
 def _seqs(shape, n, P, T, seed):
     wl = synth.Workload("t", shape, n, 1, P, T)
     prompts = synth.make_prompts(wl, seed)
@@ -119,7 +104,8 @@ def _seqs(shape, n, P, T, seed):
     return prompts, comp, np.concatenate([prompts, comp], axis=1).astype(np.int32)
 
 
-@pytest.mark.parametrize("shape,n,P,T", [(synth.TINY, 4, 16, 20), (BF16_A, 3, 40, 33), (BF16_B, 2, 64, 37)])
+@pytest.mark.parametrize("shape,n,P,T", [(synth.TINY, 4, 16, 20), (synth.TINY, 2, 7, 1), (BF16_A, 3, 40, 33),
+                                         (BF16_B, 2, 64, 37)])
 def test_teacher_forced_kl_matches_oracle(shape, n, P, T):
     """Per-position KL of two independently initialised models against the oracle, within the
     first-order effect of the forward's logits tolerance delta (twice the bound, plus 4 delta^2
@@ -144,7 +130,7 @@ def test_teacher_forced_kl_matches_oracle(shape, n, P, T):
         _, want, want_rev = opol.teacher_forced_kl(sd, w, wb, prompts[i], comp[i])
         la = om.rollout_logits(sd, w, prompts[i], comp[i])
         lb = om.rollout_logits(sd, wb, prompts[i], comp[i])
-        s, s_rev = _kl_sensitivity(la, lb)
+        s, s_rev = kl_sensitivity(la, lb)
         tol = 2 * delta * s + 4 * delta * delta
         tol_rev = 2 * delta * s_rev + 4 * delta * delta
         assert np.all(np.abs(kl[i] - want) <= tol), (i, np.abs(kl[i] - want).max(), tol.min())
