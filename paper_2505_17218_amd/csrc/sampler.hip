@@ -18,7 +18,9 @@
 // of the rest); an entry whose cheap score plus margin falls below it cannot be
 // the argmax and is skipped, every other entry gets its exact score.  The winner
 // is therefore always evaluated exactly: tokens are bit-identical to scoring
-// every entry exactly.
+// every entry exactly.  Before the cheap noise, an upper bound on the exact noise
+// read off the random word's leading ones (noise_bound) already rules out almost
+// every entry once the bound has risen, without any logarithm.
 #include "common.h"
 #include "kernels.h"
 #include "sampler_math.h"
@@ -47,6 +49,12 @@ DASH_DEV float cheap_gumbel(uint32_t x) {
 
 // Interval half-width around a cheap score sa that contains the exact score.
 DASH_DEV float screen_margin(float sa) { return kScreenTol + fabsf(sa) * (1.0f / 1048576.0f); }
+
+// Upper bound on the exact noise of the random word x, from its leading ones alone:
+// k leading ones leave u < 1 - 2^-(k+1), and -ln(1 - e) >= e gives
+// g = -ln(-ln u) < -ln(2^-(k+1)) = (k+1) ln 2 (0.6931472f is above ln 2; at most 25
+// terms, so the product's rounding stays far inside the margin added by the caller).
+DASH_DEV float noise_bound(uint32_t x) { return (float)(min(__clz(~x), 24) + 1) * 0.6931472f; }
 
 DASH_DEV float wave_max_f(float v) {
 #pragma unroll
@@ -105,6 +113,17 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
             for (int j = 0; j < 4; ++j) {
                 if (!isfinite(l[j])) continue;
                 const float sc = UNIT_T ? l[j] : div_rn(l[j], temperature);
+                // even the largest noise this word allows cannot reach the bound: skip the logs
+                const float hi = sc + noise_bound(xs[j]);
+                if (hi + screen_margin(hi) < floor_t) {
+                    if (sc > mx) {
+                        z = z * __expf(mx - sc) + 1.0f;
+                        mx = sc;
+                    } else {
+                        z += __expf(sc - mx);
+                    }
+                    continue;
+                }
                 const float sa = sc + cheap_gumbel(xs[j]);
                 const float mg = screen_margin(sa);
                 if (sa + mg >= floor_t) {
