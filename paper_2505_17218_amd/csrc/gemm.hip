@@ -410,6 +410,8 @@ bool gemm_qkv_fusable(int dtype, int n_heads, int n_kv, int head_dim) {
            (n_kv * head_dim) % 128 == 0;
 }
 
+bool gemm_qkv_fuse_pays(int M, int N) { return (long)((M + 63) / 64) * (N / 128) >= 128; }
+
 hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int K, const QkvRopeArgs& qa,
                                 hipStream_t st) {
     if (M <= 0) return hipSuccess;

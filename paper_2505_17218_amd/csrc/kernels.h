@@ -68,6 +68,10 @@ int gemm_pick_splits(int dtype, int epi, int N, int K);
 // bit.  Available for bf16 models whose q and kv column ranges are multiples of 128
 // (a 128-column tile then holds whole heads); gemm_qkv_fusable says so.
 bool gemm_qkv_fusable(int dtype, int n_heads, int n_kv, int head_dim);
+// The fused kernel's 128-column tiles leave few work-groups for small batches; it
+// pays when it has at least half a work-group per CU (the unfused GEMM plus RoPE /
+// append kernel gives the same bits, so the choice may depend on the row count).
+bool gemm_qkv_fuse_pays(int M, int N);
 hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int K, const QkvRopeArgs& qa,
                                 hipStream_t st);
 

@@ -632,7 +632,7 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
     const int sq = gemm_pick_splits(dt, EPI_STORE_F32, qr, d.d_model);
     const int so = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, hq);
     const int sd = gemm_pick_splits(dt, EPI_STORE_F32, d.d_model, d.d_ff);
-    const bool fuse_qkv = gemm_qkv_fusable(dt, d.n_heads, d.n_kv_heads, d.head_dim);
+    const bool fuse_qkv = gemm_qkv_fusable(dt, d.n_heads, d.n_kv_heads, d.head_dim) && gemm_qkv_fuse_pays(rows, qr);
     // prefill is timed as one class by its caller; per-layer classes may be limited to one layer
     int cur_layer = -1;
     auto cls = [&](int c) {

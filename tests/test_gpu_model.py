@@ -155,6 +155,30 @@ def test_bf16_swiglu_tile_regimes_bitexact():
         assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
 
 
+# q / k / v widths of 1536 / 256 / 256 (16 QKV tiles of 128 columns): a 1024-row batch runs the
+# fused QKV kernel (bias, RoPE and the KV append in the GEMM epilogue), a 40-row batch the
+# unfused GEMM and the standalone RoPE / append kernel
+BF16_F = synth.Shape("bf16-qkv2048", 1, 256, 12, 2, 128, 512, 500, 1e6, synth.DT_BF16)
+
+
+def test_bf16_fused_qkv_regimes_bitexact():
+    """Fused and unfused QKV paths give the same rows the same logits, bit for bit, in the
+    prefill (2560 vs 100 rows) and in a decode step (1024 vs 40 rows), and match the oracle."""
+    shape = BF16_F
+    w = synth.make_weights(shape, 10)
+    wl = synth.Workload("t", shape, 256, 4, 10, 2)
+    prompts = synth.make_prompts(wl, 10)
+    model = engine.Model(shape, w)
+    big = run_stepwise(model, make_kv(model, 32, 1024, 12), prompts, 4, 2, 1.0, 5)
+    small = run_stepwise(model, make_kv(model, 32, 40, 12), prompts[:10], 4, 2, 1.0, 5)
+    np.testing.assert_array_equal(small.logits[0], big.logits[0][:40])  # prefill
+    np.testing.assert_array_equal(small.logits[1], big.logits[1][:40])  # decode step
+    sd = shape_dict(shape)
+    for n in (0, 777, 1023):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], big.tokens[n])
+        assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
+
+
 def test_page_size_and_batch_invariance_bf16():
     """Page size 32 vs 64 and a different batch composition give bit-identical tokens and logits."""
     shape = BF16_B
