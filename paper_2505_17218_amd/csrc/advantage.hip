@@ -299,16 +299,17 @@ policy_loss_k(const float* __restrict__ lp, const float* __restrict__ lp_old, co
     buf[threadIdx.x] = acc;
     kbuf[threadIdx.x] = kacc;
     __syncthreads();
+    const int tid = threadIdx.x;
     for (int half = kThreads >> 1; half >= 1; half >>= 1) {
         double x = 0.0, y = 0.0;
-        if (threadIdx.x < half) {
-            x = buf[2 * threadIdx.x] + buf[2 * threadIdx.x + 1];
-            y = kbuf[2 * threadIdx.x] + kbuf[2 * threadIdx.x + 1];
+        if (tid < half) {
+            x = buf[2 * tid] + buf[2 * tid + 1];
+            y = kbuf[2 * tid] + kbuf[2 * tid + 1];
         }
         __syncthreads();
-        if (threadIdx.x < half) {
-            buf[threadIdx.x] = x;
-            kbuf[threadIdx.x] = y;
+        if (tid < half) {
+            buf[tid] = x;
+            kbuf[tid] = y;
         }
         __syncthreads();
     }

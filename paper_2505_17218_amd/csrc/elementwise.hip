@@ -47,8 +47,7 @@ template <typename T>
 __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __restrict__ tok,
                                                                const T* __restrict__ E,
                                                                const T* __restrict__ w, float* __restrict__ x,
-                                                               T* __restrict__ y, int rows, int d, int vocab,
-                                                               float eps) {
+                                                               T* __restrict__ y, int d, int vocab, float eps) {
     __shared__ float red[kRowThreads / 64];
     const int r = blockIdx.x;
     int t = tok[r];
@@ -85,7 +84,7 @@ template <typename T>
 __global__ void __launch_bounds__(kRowThreads) add_rmsnorm_k(float* __restrict__ x, const float* __restrict__ delta,
                                                              int nsplit, size_t split_stride,
                                                              const T* __restrict__ w, T* __restrict__ y,
-                                                             const int32_t* __restrict__ row_map, int rows, int d,
+                                                             const int32_t* __restrict__ row_map, int d,
                                                              float eps, int write_x) {
     __shared__ float red[kRowThreads / 64];
     const int i_out = blockIdx.x;
@@ -232,10 +231,10 @@ hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, co
     const unsigned blocks = (unsigned)rows;
     if (dtype == 1)
         embed_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(tok, (const bf16_t*)E, (const bf16_t*)w, x,
-                                                                (bf16_t*)y, rows, d, vocab, eps);
+                                                                (bf16_t*)y, d, vocab, eps);
     else
         embed_rmsnorm_k<float><<<blocks, kRowThreads, 0, st>>>(tok, (const float*)E, (const float*)w, x, (float*)y,
-                                                               rows, d, vocab, eps);
+                                                               d, vocab, eps);
     return hipGetLastError();
 }
 
@@ -247,10 +246,10 @@ hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nspli
     const unsigned blocks = (unsigned)rows;
     if (dtype == 1)
         add_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const bf16_t*)w,
-                                                              (bf16_t*)y, row_map, rows, d, eps, write_x);
+                                                              (bf16_t*)y, row_map, d, eps, write_x);
     else
         add_rmsnorm_k<float><<<blocks, kRowThreads, 0, st>>>(x, delta, nsplit, split_stride, (const float*)w,
-                                                             (float*)y, row_map, rows, d, eps, write_x);
+                                                             (float*)y, row_map, d, eps, write_x);
     return hipGetLastError();
 }
 
