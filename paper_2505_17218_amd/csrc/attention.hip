@@ -31,7 +31,7 @@ namespace dash {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBufferDword3 = 0x00020000;
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family): out-of-range reads give 0
 // Cache policies of the K/V block loads.  Decode streams (non-temporal) the blocks
 // that only one row reads: measured on gfx950 with the last-level cache cold, the
 // plain policy streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.
@@ -40,7 +40,7 @@ constexpr int kBufferDword3 = 0x00020000;
 // Prefill keeps the default: each key block is read again by every 16-query column
 // block of its sequence and should stay cached (streaming it measured 1.75x slower).
 constexpr int kKvStream = 2, kKvReuse = 0;
-constexpr int kMaxGroupWaves = 16;  // samples per group served by one workgroup  // raw buffer resource word 3 (gfx9 family): out-of-range reads give 0
+constexpr int kMaxGroupWaves = 16;  // samples per group served by one workgroup
 
 // ---- shared MFMA block step ---------------------------------------------
 // A wave attends 16 "columns" (decode: the query heads of one GQA group;
