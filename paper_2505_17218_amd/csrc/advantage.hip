@@ -239,14 +239,9 @@ live_compact_k(const int32_t* __restrict__ tok, const int32_t* __restrict__ slot
     if (threadIdx.x == 0) *count = base;
 }
 
-// Policy-gradient loss of the kept samples, float64: sample n's sequence
-// log-prob is the sum of its first len[n] token log-probs (in order), and
-// loss = -(1/n_total) sum_k A[kept[k]] * seqlp[kept[k]] with the k-sum split
-// over threads in a fixed assignment (k = t, t + kThreads, ...) and merged by a
-// pairwise LDS tree, so the result is reproducible bit for bit.
-// Loss over the kept samples, float64.  Each thread takes kept samples k, k + 256, ...
-// and sums a sample's per-token values in token order; the 256 partials are then
-// added as a pairwise tree.  Surrogate: A S (PG, no old log-probs) or PPO's
+// Loss over the kept samples, float64, reproducible bit for bit.  Each thread takes
+// kept samples k, k + 256, ... and sums a sample's per-token values in token order;
+// the 256 partials are then added as a pairwise tree.  Surrogate: A S (PG, no old log-probs) or PPO's
 // min(rho A, clip(rho, 1 - eps, 1 + eps) A) with rho = exp(S - S_old); the KL sums
 // (if given) enter with weight beta.  stats[4 n ..] = (S, S_old, KL, dloss/dS).
 __global__ void __launch_bounds__(kThreads)
