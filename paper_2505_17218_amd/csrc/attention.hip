@@ -465,24 +465,75 @@ __global__ void __launch_bounds__(64) prefill_attn_bf16_k(const bf16_t* __restri
 }
 
 // Merge the context splits of rows that have more than one, in split order:
-// o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
-template <typename T>
-__global__ void combine_k(const float* __restrict__ part, const int32_t* __restrict__ pos, int rows, int n_heads,
-                          int max_splits, int split_keys, int hd, T* __restrict__ o) {
+// o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.  One wave per (row, head), a
+// lane per output dim (two for hd = 128).  Up to MS splits every load is issued
+// before any arithmetic (the row's split count only masks which values enter), so a
+// merge costs one memory round trip instead of three dependent ones; loads of
+// splits past the row's count stay inside the partial buffer and are never used.
+template <typename T, int MS>
+__global__ void __launch_bounds__(64) combine_k(const float* __restrict__ part, const int32_t* __restrict__ pos,
+                                                int rows, int n_heads, int max_splits, int split_keys, int hd,
+                                                T* __restrict__ o) {
     const int rh = blockIdx.x;  // row * n_heads + head
     const int row = rh / n_heads;
-    const int ns = min((pos[row] + split_keys) / split_keys, max_splits);  // ceil((pos + 1) / split keys)
-    if (ns <= 1) return;  // written directly by the attention kernel
+    const int d0 = threadIdx.x, d1 = threadIdx.x + 64;
+    const bool two = d1 < hd;
     const float* ml = part + (size_t)rows * n_heads * max_splits * hd + (size_t)rh * max_splits * 2;
+    const float* pr = part + (size_t)rh * max_splits * hd;
+    const int p = pos[row];
+    float mv[MS], lv[MS], x0[MS], x1[MS];
+#pragma unroll
+    for (int s = 0; s < MS; ++s) {
+        mv[s] = lv[s] = x0[s] = x1[s] = 0.f;
+        if (s < max_splits) {
+            mv[s] = ml[2 * s];
+            lv[s] = ml[2 * s + 1];
+            x0[s] = pr[(size_t)s * hd + d0];
+            x1[s] = two ? pr[(size_t)s * hd + d1] : 0.f;
+        }
+    }
+    const int ns = min((p + split_keys) / split_keys, max_splits);  // ceil((pos + 1) / split keys)
+    if (ns <= 1) return;  // written directly by the attention kernel
+    float M = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < MS; ++s)
+        if (s < ns) M = fmaxf(M, mv[s]);
+    float den = 0.f, n0 = 0.f, n1 = 0.f;
+#pragma unroll
+    for (int s = 0; s < MS; ++s) {
+        if (s < ns) {
+            const float w = exp2f(mv[s] - M);
+            den += w * lv[s];
+            n0 += w * x0[s];
+            n1 += w * x1[s];
+        }
+    }
+    const float inv = den > 0.f ? 1.0f / den : 0.f;
+    st_elem(o + (size_t)rh * hd + d0, n0 * inv);
+    if (two) st_elem(o + (size_t)rh * hd + d1, n1 * inv);
+}
+
+// The same merge for rows with more splits than combine_k unrolls (loads per split).
+template <typename T>
+__global__ void __launch_bounds__(64) combine_many_k(const float* __restrict__ part, const int32_t* __restrict__ pos,
+                                                     int rows, int n_heads, int max_splits, int split_keys, int hd,
+                                                     T* __restrict__ o) {
+    const int rh = blockIdx.x;
+    const int row = rh / n_heads;
+    const int ns = min((pos[row] + split_keys) / split_keys, max_splits);
+    if (ns <= 1) return;
+    const float* ml = part + (size_t)rows * n_heads * max_splits * hd + (size_t)rh * max_splits * 2;
+    const float* pr = part + (size_t)rh * max_splits * hd;
     float M = -INFINITY;
     for (int s = 0; s < ns; ++s) M = fmaxf(M, ml[2 * s]);
-    float den = 0.f;
-    for (int s = 0; s < ns; ++s) den += exp2f(ml[2 * s] - M) * ml[2 * s + 1];
-    const float inv = den > 0.f ? 1.0f / den : 0.f;
-    for (int d = threadIdx.x; d < hd; d += blockDim.x) {
-        float num = 0.f;
-        for (int s = 0; s < ns; ++s) num += exp2f(ml[2 * s] - M) * part[((size_t)rh * max_splits + s) * hd + d];
-        st_elem(o + (size_t)rh * hd + d, num * inv);
+    for (int d = threadIdx.x; d < hd; d += 64) {
+        float den = 0.f, num = 0.f;
+        for (int s = 0; s < ns; ++s) {
+            const float w = exp2f(ml[2 * s] - M);
+            den += w * ml[2 * s + 1];
+            num += w * pr[(size_t)s * hd + d];
+        }
+        st_elem(o + (size_t)rh * hd + d, num * (den > 0.f ? 1.0f / den : 0.f));
     }
 }
 
@@ -621,8 +672,14 @@ hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int
                                     int max_ctx, int split_keys, const float* ws_part, void* o, hipStream_t st) {
     const int ms = (max_ctx + split_keys - 1) / split_keys;
     if (dtype != 1 || ms <= 1 || rows <= 0) return hipSuccess;
-    combine_k<bf16_t><<<rows * n_heads, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, split_keys, head_dim,
-                                                     (bf16_t*)o);
+    if (head_dim != 64 && head_dim != 128) return hipErrorInvalidValue;
+    const int grid = rows * n_heads;
+    if (ms <= 8)
+        combine_k<bf16_t, 8><<<grid, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, split_keys, head_dim, (bf16_t*)o);
+    else if (ms <= 16)
+        combine_k<bf16_t, 16><<<grid, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, split_keys, head_dim, (bf16_t*)o);
+    else
+        combine_many_k<bf16_t><<<grid, 64, 0, st>>>(ws_part, pos, rows, n_heads, ms, split_keys, head_dim, (bf16_t*)o);
     return hipGetLastError();
 }
 

@@ -93,6 +93,24 @@ def test_bf16_split_length_follows_capacity(max_seqs, split):
     print(f"split {split}: max |dlogits| = {worst:.3g}")
 
 
+@pytest.mark.parametrize("P,n_splits", [(2600, 11), (4400, 18)])
+def test_bf16_many_attention_splits(P, n_splits):
+    """A small cache keeps 256-key splits, so long contexts are merged from many splits:
+    11 (the merge with every load issued up front, up to 16 splits) and 18 (the merge
+    that loads split by split).  Both match the oracle."""
+    shape = BF16_A
+    w = synth.make_weights(shape, 1)
+    T = 3
+    wl = synth.Workload("t", shape, 1, 2, P, T)
+    prompts = synth.make_prompts(wl, 1)
+    model = engine.Model(shape, w)
+    kv = engine.KVCache(model, 32, 4, P + T, 2 * ((P + T + 31) // 32) + 8)
+    assert kv.split_keys == 256 and -(-(P + T) // 256) == n_splits
+    run = run_stepwise(model, kv, prompts, 2, T, 1.0, 77)
+    worst = _check_run(shape, w, prompts, 2, T, run, 1.0, 77, TOL[shape.dtype])
+    print(f"P={P} ({n_splits} splits): max |dlogits| = {worst:.3g}")
+
+
 def test_bf16_large_batch_gemm_tiles():
     """160 decode rows (M > 128 with a tail) through the MFMA GEMMs; checked on sampled rows."""
     shape = BF16_A
