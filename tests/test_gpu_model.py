@@ -76,10 +76,10 @@ def test_bf16_stepwise_matches_oracle(shape, n_prompts, G, P, T):
     print(f"{shape.name} P={P} T={T}: max |dlogits| = {worst:.3g}")
 
 
-@pytest.mark.parametrize("max_seqs,split", [(4, 256), (1024, 1024)])
+@pytest.mark.parametrize("max_seqs,split", [(4, 128), (1024, 1024)])
 def test_bf16_split_length_follows_capacity(max_seqs, split):
     """The decode-attention split length is fixed per cache from its capacity: a small
-    cache cuts a 600-key context into 256-key splits merged by the combine kernel, a
+    cache cuts a 600-key context into 128-key splits merged by the combine kernel, a
     large one reads it as a single 1024-key split.  Both match the oracle."""
     shape = BF16_A
     w = synth.make_weights(shape, 1)
@@ -93,10 +93,10 @@ def test_bf16_split_length_follows_capacity(max_seqs, split):
     print(f"split {split}: max |dlogits| = {worst:.3g}")
 
 
-@pytest.mark.parametrize("P,n_splits", [(2600, 11), (4400, 18)])
+@pytest.mark.parametrize("P,n_splits", [(1800, 15), (2600, 21)])
 def test_bf16_many_attention_splits(P, n_splits):
-    """A small cache keeps 256-key splits, so long contexts are merged from many splits:
-    11 (the merge with every load issued up front, up to 16 splits) and 18 (the merge
+    """A small cache keeps 128-key splits, so long contexts are merged from many splits:
+    15 (the merge with every load issued up front, up to 16 splits) and 21 (the merge
     that loads split by split).  Both match the oracle."""
     shape = BF16_A
     w = synth.make_weights(shape, 1)
@@ -105,7 +105,7 @@ def test_bf16_many_attention_splits(P, n_splits):
     prompts = synth.make_prompts(wl, 1)
     model = engine.Model(shape, w)
     kv = engine.KVCache(model, 32, 4, P + T, 2 * ((P + T + 31) // 32) + 8)
-    assert kv.split_keys == 256 and -(-(P + T) // 256) == n_splits
+    assert kv.split_keys == 128 and -(-(P + T) // 128) == n_splits
     run = run_stepwise(model, kv, prompts, 2, T, 1.0, 77)
     worst = _check_run(shape, w, prompts, 2, T, run, 1.0, 77, TOL[shape.dtype])
     print(f"P={P} ({n_splits} splits): max |dlogits| = {worst:.3g}")
