@@ -450,7 +450,7 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                 return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
-        if (M <= 256 || (K >= 4096 && M <= 512)) {
+        if (M <= 256) {
             // Few work-groups stream the weights here; four k-steps in flight per
             // thread instead of two pull them faster while the launch is small (unsplit
             // K, or one 64-row block): measured 22-28% faster on the 1.5B and 3B QKV / O
@@ -460,16 +460,22 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                 return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<64, 32, 2, 1, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
-        // Larger batches: the largest tile that still gives the launch enough work-groups
-        // (measured crossovers on the 1.5B and 3B shapes: the split down projection
-        // 128x256 -> 256x256 past 1024 rows, 12-18% faster from 1536; QKV / O 64x64 ->
-        // 128x128 past 1024 rows, 4-30% faster at 1536-4096, -> 256x256 past 4096, 15-26%
-        // faster at 8192-16384).
+        // Larger batches: the largest tile that still gives the launch enough work-groups.
+        // Measured crossovers on the 0.5B, 1.5B and 3B shapes: the split down projection
+        // 64x64 up to 384 rows (12-15% faster than 128x256 there), 128x256 up to 1024,
+        // 256x256 past that (12-18% faster from 1536 rows); QKV / O 64x64 with three
+        // k-steps in flight up to 512 rows (10-15% faster than two), 64x64 up to 1024,
+        // 128x128 up to 4096 (4-30% faster from 1536), 256x256 past that (15-26% faster
+        // at 8192-16384).
         if (K >= 4096) {
-            if (M > 1024)
-                return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
-            return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            if (M <= 384)
+                return run_bf16<64, 64, 2, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            if (M <= 1024)
+                return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
+        if (M <= 512)
+            return run_bf16<64, 64, 2, 2, 3, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         if (M <= 1024)  // decode QKV / O: unsplit, small tiles fill the GPU
             return run_bf16<64, 64, 2, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         if (M <= 4096)

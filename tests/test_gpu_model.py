@@ -177,27 +177,27 @@ def test_bf16_swiglu_tile_regimes_bitexact():
 # k-steps in flight up to 64 rows, on 64x64 tiles at 65-128 rows, on 64x128 tiles with two
 # k-steps in flight at 129-256 rows, on 128x128 tiles up to 1024 rows and on 256x256 past
 # that; the down projection (K = 8192, split) on 64x32 tiles four or two k-steps ahead,
-# 128x256 or 256x256; the output projection on 64x32, 64x64, 128x128 or 256x256 tiles
+# 64x64, 128x256 or 256x256; the output projection on 64x32 tiles, 64x64 tiles three or
+# two k-steps ahead, 128x128 or 256x256 tiles
 BF16_G = synth.Shape("bf16-ff8192", 1, 256, 4, 2, 64, 8192, 500, 1e6, synth.DT_BF16)
 
 
 def test_bf16_gemm_regimes_across_batch_sizes_bitexact():
-    """Batches of 10, 25, 50, 256 and 512 prompts (prefill 100 / 250 / 500 / 2560 / 5120
-    rows, decode 40 / 100 / 200 / 1024 / 2048 rows) run different gate/up, down and output
-    projection tilings; the rows they share get the same logits bit for bit, and sampled
-    rows match the oracle."""
+    """Batches of 10 to 512 prompts (prefill 100 to 5120 rows, decode 40 to 2048 rows) run
+    every gate/up, down and output projection tiling; the rows they share get the same
+    logits bit for bit, and sampled rows match the oracle."""
     shape = BF16_G
     w = synth.make_weights(shape, 11)
     wl = synth.Workload("t", shape, 512, 4, 10, 2)
     prompts = synth.make_prompts(wl, 11)
     model = engine.Model(shape, w)
     runs = {n: run_stepwise(model, make_kv(model, 32, 4 * n, 12), prompts[:n], 4, 2, 1.0, 5)
-            for n in (10, 25, 50, 256, 512)}
-    for n in (25, 50, 256, 512):
+            for n in (10, 25, 50, 75, 120, 256, 512)}
+    for n in (25, 50, 75, 120, 256, 512):
         np.testing.assert_array_equal(runs[10].logits[0], runs[n].logits[0][:40])  # prefill
         np.testing.assert_array_equal(runs[10].logits[1], runs[n].logits[1][:40])  # decode step
     sd = shape_dict(shape)
-    for n_prompts, n in ((10, 0), (25, 99), (50, 199), (256, 1023), (512, 2047)):
+    for n_prompts, n in ((10, 0), (25, 99), (50, 199), (75, 299), (120, 479), (256, 1023), (512, 2047)):
         run = runs[n_prompts]
         ref = om.rollout_logits(sd, w, prompts[n // 4], run.tokens[n])
         assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype], (n_prompts, n)
