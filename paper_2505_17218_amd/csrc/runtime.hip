@@ -303,7 +303,9 @@ struct Ws {
 };
 
 // max_ctx bounds the decode attention's context splits (0: no decode use).
-Ws plan_ws(const dash_model* m, int max_rows, char* base, int max_ctx) {
+// decode_rows (default max_rows) sizes the decode-attention partials: a rollout's step
+// workspace also serves the prefill's larger row count, which needs none.
+Ws plan_ws(const dash_model* m, int max_rows, char* base, int max_ctx, int decode_rows = -1) {
     const auto& d = m->d;
     const size_t e = m->esz;
     size_t off = 0;
@@ -325,7 +327,8 @@ Ws plan_ws(const dash_model* m, int max_rows, char* base, int max_ctx) {
     w.delta = (float*)take((size_t)std::max(so, sd) * R * d.d_model * 4);
     w.h = take(R * d.d_ff * e);
     w.cs = (float*)take(R * d.head_dim * 4);
-    w.attn_part = (float*)take(attention_partial_floats(max_rows, d.n_heads, d.head_dim, max_ctx) * 4);
+    w.attn_part = (float*)take(
+        attention_partial_floats(decode_rows < 0 ? max_rows : decode_rows, d.n_heads, d.head_dim, max_ctx) * 4);
     w.pos = (int32_t*)take(R * 4);
     w.slot = (int32_t*)take(R * 4);
     w.pslot = (int32_t*)take(R * 4);
@@ -748,8 +751,10 @@ int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prom
     if (need > kv->free_list.size())
         return fail(DASH_ECAPACITY, "pool exhausted: prefill needs %zu pages, %zu free", need, kv->free_list.size());
     const int rows_fit = ws_rows_for(m, ws_bytes, n_prompts * P);
-    const int chunk = rows_fit / P;
+    int chunk = rows_fit / P;
     if (chunk < 1) return fail(DASH_ECAPACITY, "workspace cannot hold one prompt of %d tokens", P);
+    const int n_chunks = (n_prompts + chunk - 1) / chunk;
+    chunk = (n_prompts + n_chunks - 1) / n_chunks;  // as many chunks, of equal size (the last may be smaller)
     // host bookkeeping: pages of every sample's slot
     std::vector<int32_t> pairs;
     for (int p = 0; p < n_prompts; ++p) {
@@ -943,7 +948,7 @@ RolloutWs plan_rollout(const dash_model* m, int n_prompts, int P, int G, int max
     const int prefill_rows = std::min(n_prompts, std::max(1, 16384 / std::max(1, P))) * P;
     const int rows = std::max(N, prefill_rows);
     RolloutWs r{};
-    r.step = plan_ws(m, rows, base, max_ctx);
+    r.step = plan_ws(m, rows, base, max_ctx, N);
     size_t off = r.step.bytes;
     auto take = [&](size_t bytes) {
         char* p = base ? base + off : nullptr;
