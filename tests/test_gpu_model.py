@@ -111,6 +111,26 @@ def test_bf16_many_attention_splits(P, n_splits):
     print(f"P={P} ({n_splits} splits): max |dlogits| = {worst:.3g}")
 
 
+def test_prefill_in_chunks_is_bit_identical():
+    """A workspace for 5 prompts makes dash_prefill take 8 prompts in two equal chunks of 4;
+    the logits, and a decode step over the cache it wrote, match a one-chunk prefill bit for bit."""
+    shape, G, P = BF16_A, 2, 40
+    w = synth.make_weights(shape, 12)
+    prompts = synth.make_prompts(synth.Workload("t", shape, 8, G, P, 2), 12)
+    model = engine.Model(shape, w)
+    slots = list(range(8 * G))
+    outs = []
+    for ws in (None, model.workspace(5 * P, 0)):
+        kv = make_kv(model, 32, 8 * G, P + 1)
+        logits = engine.prefill(model, kv, dev_i32(prompts), G, slots, ws=ws).cpu().numpy()
+        L.dash_kv_reserve(kv.handle, slots, P + 1, engine.stream_handle())
+        tok = dev_i32(np.arange(8 * G) % shape.vocab)
+        step = engine.decode_step(model, kv, tok, dev_i32(np.arange(8 * G)), dev_i32(np.full(8 * G, P)))
+        outs.append((logits, step.cpu().numpy()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
 def test_bf16_large_batch_gemm_tiles():
     """160 decode rows (M > 128 with a tail) through the MFMA GEMMs; checked on sampled rows."""
     shape = BF16_A
