@@ -149,10 +149,6 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
     const int hd = g.head_dim, half = hd >> 1, n_kv = g.n_kv;
     const int qkv_rows = (n_heads + 2 * n_kv) * hd;
     const float* row = qkv + (size_t)r * qkv_rows;
-    const int p = pos[r];
-    const int page = kv_page_of(g, page_table, slot[r], p);
-    if (page < 0 && blockIdx.y == 0 && threadIdx.x == 0 && status) atomicOr(status, 1u);
-    const int key = p % g.page_size;
     auto val = [&](int j) {
         float v = row[j];
         for (int s = 1; s < nsplit; ++s) v += row[s * split_stride + j];
@@ -160,13 +156,29 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
     };
     const int n_rope = (n_heads + n_kv) * half;
     const int it = blockIdx.y * blockDim.x + threadIdx.x;
-    if (it < n_rope) {
-        const int h = it / half, i = it - h * half;
+    // The operands are read before the cache page is looked up (position and slot,
+    // then the page table), so the two chains of loads overlap.
+    const bool is_rope = it < n_rope, is_v = !is_rope && it < n_rope + n_kv * hd;
+    const int h = is_rope ? it / half : (it - n_rope) / hd;
+    const int i = is_rope ? it - h * half : (it - n_rope) - h * hd;  // pair index / v dim
+    float a = 0.f, b = 0.f, c = 1.f, sn = 0.f;
+    if (is_rope) {
         const int j = h * hd + i;
-        const float a = val(j), b = val(j + half);
+        a = val(j);
+        b = val(j + half);
         const float* c_s = cs + ((size_t)r * half + i) * 2;
+        c = c_s[0];
+        sn = c_s[1];
+    } else if (is_v) {
+        a = val((n_heads + n_kv) * hd + (it - n_rope));
+    }
+    const int p = pos[r];
+    const int page = kv_page_of(g, page_table, slot[r], p);
+    if (page < 0 && blockIdx.y == 0 && threadIdx.x == 0 && status) atomicOr(status, 1u);
+    const int key = p % g.page_size;
+    if (is_rope) {
         float lo, hi;
-        rope_pair(a, b, c_s[0], c_s[1], lo, hi);
+        rope_pair(a, b, c, sn, lo, hi);
         if (h < n_heads) {
             T* q = q_out + ((size_t)r * n_heads + h) * hd;
             st_elem(q + i, lo);
@@ -176,12 +188,9 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
             st_elem(kb + k_index<T>(g, key, i), lo);
             st_elem(kb + k_index<T>(g, key, i + half), hi);
         }
-    } else if (it < n_rope + n_kv * hd && page >= 0) {
-        const int jj = it - n_rope;
-        const int h = jj / hd, dd = jj - h * hd;
-        const float v = val((n_heads + n_kv) * hd + jj);
+    } else if (is_v && page >= 0) {
         T* vb = pool + kv_block(g, layer, page, h, 1);
-        st_elem(vb + v_index<T>(g, key, dd), v);
+        st_elem(vb + v_index<T>(g, key, i), a);
     }
 }
 
