@@ -194,7 +194,8 @@ int dash_kv_device_status(dash_kv* kv, uint32_t* out, void* stream);
 
 /* Bytes of device workspace dash_prefill / dash_decode_step need for up to
  * max_rows token rows per call (prefill rows = prompts in one chunk x prompt
- * length; prefill splits larger batches into chunks of whole prompts).
+ * length; prefill splits a batch the workspace cannot hold at once into the
+ * fewest chunks of whole prompts, of equal size but for a smaller last one).
  * max_ctx: the max_ctx of the kv handle used with it (sizes the decode
  * attention's per-split partial results; 0 for a prefill-only workspace). */
 size_t dash_workspace_bytes(const dash_model* model, int32_t max_rows, int32_t max_ctx);
