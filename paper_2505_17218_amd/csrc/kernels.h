@@ -84,12 +84,12 @@ hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int 
 // 128 rather than 256: measured 10% less attention time for 64 sequences of the 3B
 // shape (contexts 513-1536), the merge cost unchanged.
 constexpr int kAttnMinSplitKeys = 128;
-constexpr int kAttnTargetWaves = 2048;  // 2 waves per SIMD over 256 CUs
+constexpr int kAttnTargetWaves = 2048;  // 2 waves per SIMD over 256 CUs (hd 128; 3 per SIMD for hd 64)
 // Split length for a cache: the largest power of two >= kAttnMinSplitKeys whose
 // split count still gives max_seqs * n_kv * splits >= kAttnTargetWaves at max_ctx
 // (and no longer than max_ctx needs).  Long splits mean fewer partials to write and
 // merge; short ones give small batches enough waves.
-int attention_split_keys(int max_seqs, int n_kv, int max_ctx);
+int attention_split_keys(int max_seqs, int n_kv, int max_ctx, int head_dim);
 hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos, const int32_t* slot,
                                    const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                    int n_heads, void* o, int rows, int max_ctx, float* ws_part, hipStream_t st);

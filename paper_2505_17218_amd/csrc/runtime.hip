@@ -429,7 +429,7 @@ int dash_kv_create(const dash_model* m, void* pool, size_t pool_bytes, int32_t p
     kv->max_ctx = max_ctx;
     const int max_pages = (max_ctx + ps - 1) / ps;
     kv->g = KVGeom{m->d.n_layers, (int)pages, m->d.n_kv_heads, m->d.head_dim, ps, max_pages, max_seqs,
-                   attention_split_keys(max_seqs, m->d.n_kv_heads, max_ctx), 0};
+                   attention_split_keys(max_seqs, m->d.n_kv_heads, max_ctx, m->d.head_dim), 0};
     const size_t ent = table_entries(max_seqs, max_ctx, ps);
     kv->d_table = (int32_t*)d_table;
     kv->d_status = (uint32_t*)((char*)d_table + align_up(ent * 4, 256));

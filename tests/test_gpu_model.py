@@ -76,11 +76,12 @@ def test_bf16_stepwise_matches_oracle(shape, n_prompts, G, P, T):
     print(f"{shape.name} P={P} T={T}: max |dlogits| = {worst:.3g}")
 
 
-@pytest.mark.parametrize("max_seqs,split", [(4, 128), (1024, 1024)])
+@pytest.mark.parametrize("max_seqs,split", [(4, 128), (1024, 512), (2048, 1024)])
 def test_bf16_split_length_follows_capacity(max_seqs, split):
-    """The decode-attention split length is fixed per cache from its capacity: a small
-    cache cuts a 600-key context into 128-key splits merged by the combine kernel, a
-    large one reads it as a single 1024-key split.  Both match the oracle."""
+    """The decode-attention split length is fixed per cache from its capacity (head dim 64:
+    three waves per SIMD): a small cache cuts a 600-key context into 128-key splits merged
+    by the combine kernel, a larger one into two 512-key splits, a large one reads it as a
+    single 1024-key split.  All match the oracle."""
     shape = BF16_A
     w = synth.make_weights(shape, 1)
     wl = synth.Workload("t", shape, 2, 2, 600, 6)
