@@ -450,24 +450,23 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                 return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
-        if (M <= 256) {
-            // Few work-groups stream the weights here; four k-steps in flight per
-            // thread instead of two pull them faster while the launch is small (unsplit
-            // K, or one 64-row block): measured 22-28% faster on the 1.5B and 3B QKV / O
-            // shapes up to 256 rows and on the split down projection up to 64 rows, no
-            // gain for the split projection past that.
-            if (K < 4096 || M <= 64)
-                return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
-            return run_bf16<64, 32, 2, 1, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        if (M <= 256 && (K < 4096 || M <= 64)) {
+            // Few work-groups stream the weights here; four k-steps in flight per thread
+            // instead of two pull them faster while the launch is small (unsplit K, or one
+            // 64-row block): measured 22-28% faster on the 1.5B and 3B QKV / O shapes up to
+            // 256 rows and on the split down projection up to 64 rows.
+            return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
         // Larger batches: the largest tile that still gives the launch enough work-groups.
         // Measured crossovers on the 0.5B, 1.5B and 3B shapes: the split down projection
-        // 64x64 up to 384 rows (12-15% faster than 128x256 there), 128x256 up to 1024,
-        // 256x256 past that (12-18% faster from 1536 rows); QKV / O 64x64 with three
-        // k-steps in flight up to 512 rows (10-15% faster than two), 64x64 up to 1024,
-        // 128x128 up to 4096 (4-30% faster from 1536), 256x256 past that (15-26% faster
-        // at 8192-16384).
+        // 64x64 three k-steps ahead up to 128 rows and two up to 384 (12-19% faster than
+        // 64x32 there), 128x256 up to 1024, 256x256 past that (12-18% faster from 1536
+        // rows); QKV / O 64x64 three k-steps ahead up to 512 rows (10-15% faster than two),
+        // 64x64 up to 1024, 128x128 up to 4096 (4-30% faster from 1536), 256x256 past that
+        // (15-26% faster at 8192-16384).
         if (K >= 4096) {
+            if (M <= 128)
+                return run_bf16<64, 64, 2, 2, 3, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             if (M <= 384)
                 return run_bf16<64, 64, 2, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             if (M <= 1024)

@@ -197,9 +197,9 @@ def test_bf16_swiglu_tile_regimes_bitexact():
 # d_ff = 8192 (128 SwiGLU tiles of 64 column pairs): gate/up runs on 64x128 tiles with three
 # k-steps in flight up to 64 rows, on 64x64 tiles at 65-128 rows, on 64x128 tiles with two
 # k-steps in flight at 129-256 rows, on 128x128 tiles up to 1024 rows and on 256x256 past
-# that; the down projection (K = 8192, split) on 64x32 tiles four or two k-steps ahead,
-# 64x64, 128x256 or 256x256; the output projection on 64x32 tiles, 64x64 tiles three or
-# two k-steps ahead, 128x128 or 256x256 tiles
+# that; the down projection (K = 8192, split) on 64x32 tiles four k-steps ahead, 64x64
+# tiles three or two k-steps ahead, 128x256 or 256x256; the output projection on 64x32
+# tiles, 64x64 tiles three or two k-steps ahead, 128x128 or 256x256 tiles
 BF16_G = synth.Shape("bf16-ff8192", 1, 256, 4, 2, 64, 8192, 500, 1e6, synth.DT_BF16)
 
 
