@@ -445,9 +445,11 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             }
             return run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
         }
-        if (N >= 8192) {  // LM head: many tiles, the largest tile wins
+        if (N >= 8192) {  // LM head: many tiles, the largest tile that the batch fills wins
             if (M <= 64)
                 return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            if (M <= 128)  // measured 10-18% faster than 256x256 at 96-128 rows
+                return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
         if (M <= 256 && (K < 4096 || M <= 64)) {

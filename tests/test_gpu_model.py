@@ -224,6 +224,30 @@ def test_bf16_gemm_regimes_across_batch_sizes_bitexact():
         assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype], (n_prompts, n)
 
 
+# vocab 9000 (>= 8192 columns: the LM head's tiles): 64x256 up to 64 rows, 128x256 up to 128,
+# 256x256 past that
+BF16_H = synth.Shape("bf16-v9000", 1, 256, 4, 2, 64, 512, 9000, 1e6, synth.DT_BF16)
+
+
+def test_bf16_lm_head_regimes_bitexact():
+    """Batches of 10, 25 and 75 prompts put the LM head on 64x256, 128x256 and 256x256 tiles
+    (prefill 10 / 25 / 75 rows, decode 40 / 100 / 300 rows); the rows they share get the same
+    logits bit for bit, and sampled rows match the oracle."""
+    shape = BF16_H
+    w = synth.make_weights(shape, 14)
+    prompts = synth.make_prompts(synth.Workload("t", shape, 75, 4, 10, 2), 14)
+    model = engine.Model(shape, w)
+    runs = {n: run_stepwise(model, make_kv(model, 32, 4 * n, 12), prompts[:n], 4, 2, 1.0, 5) for n in (10, 25, 75)}
+    for n in (25, 75):
+        np.testing.assert_array_equal(runs[10].logits[0], runs[n].logits[0][:40])  # prefill
+        np.testing.assert_array_equal(runs[10].logits[1], runs[n].logits[1][:40])  # decode step
+    sd = shape_dict(shape)
+    for n_prompts, n in ((10, 0), (25, 99), (75, 299)):
+        run = runs[n_prompts]
+        ref = om.rollout_logits(sd, w, prompts[n // 4], run.tokens[n])
+        assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype], (n_prompts, n)
+
+
 # q / k / v widths of 1536 / 256 / 256 (16 QKV tiles of 128 columns): a 1024-row batch runs the
 # fused QKV kernel (bias, RoPE and the KV append in the GEMM epilogue), a 40-row batch the
 # unfused GEMM and the standalone RoPE / append kernel
