@@ -36,6 +36,71 @@ ATTN_TRAFFIC = {
 }
 
 
+class SclkSampler:
+    """The shader clock the driver reports for this GPU (the current level of its
+    pp_dpm_sclk), sampled every `period` seconds on a background thread while the timed
+    steps run: observed, not pinned.  `result()` is None where the file is unavailable."""
+
+    def __init__(self, period: float = 0.05):
+        import glob
+        import re
+        import threading
+
+        self.re = re.compile(r"(\d+)\s*mhz", re.IGNORECASE)
+        self.period, self.samples, self.stop = period, [], threading.Event()
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if len(paths) == 1 else self._match(paths)
+        self.thread = threading.Thread(target=self._run, daemon=True)
+
+    @staticmethod
+    def _match(paths):
+        # several cards visible: the one whose PCI bus is torch's device 0
+        try:
+            import torch
+
+            bus = "%02x:" % torch.cuda.get_device_properties(0).pci_bus_id
+            for p in paths:
+                if os.path.basename(os.path.realpath(os.path.dirname(p))).split(":", 1)[-1].startswith(bus):
+                    return p
+        except Exception:
+            pass
+        return None
+
+    def _read(self):
+        with open(self.path) as f:
+            for line in f:
+                if "*" in line:
+                    m = self.re.search(line)
+                    return int(m.group(1)) if m else None
+        return None
+
+    def _run(self):
+        while not self.stop.is_set():
+            try:
+                v = self._read()
+                if v:
+                    self.samples.append(v)
+            except OSError:
+                return
+            self.stop.wait(self.period)
+
+    def __enter__(self):
+        if self.path:
+            self.thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self.stop.set()
+        if self.thread.is_alive():
+            self.thread.join()
+
+    def result(self):
+        if not self.samples:
+            return None
+        v = sorted(self.samples)
+        return {"median": v[len(v) // 2], "max": v[-1], "samples": len(v), "source": "pp_dpm_sclk"}
+
+
 def measured_attention_traffic(workload: str):
     """The counted bytes per attention launch, or None if the workload or the kernel sources differ."""
     import hashlib
@@ -246,16 +311,17 @@ def main() -> int:
     L.dash_profile_enable((1 << L.K["attn"]) | (1 << L.K["attn_combine"]) | (1 << L.K["prefill"]))
     L.dash_profile_layer(prof_layer)
     torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    step_ms = []
-    for i in range(args.steps):
-        t_i = time.perf_counter()
-        _, kept = step()
+    with SclkSampler() as sclk:
+        t_start = time.perf_counter()
+        step_ms = []
+        for i in range(args.steps):
+            t_i = time.perf_counter()
+            _, kept = step()
+            torch.cuda.synchronize()
+            step_ms.append((time.perf_counter() - t_i) * 1e3)
+            log(f"step {i}: {time.perf_counter() - t_start:.2f} s cumulative")
         torch.cuda.synchronize()
-        step_ms.append((time.perf_counter() - t_i) * 1e3)
-        log(f"step {i}: {time.perf_counter() - t_start:.2f} s cumulative")
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+        elapsed = time.perf_counter() - t_start
     timed = L.dash_profile_read(reset=True)
     L.dash_profile_enable(0)
     L.dash_profile_layer(-1)
@@ -356,6 +422,7 @@ def main() -> int:
         "gemm_mfma": gemm,
         "prefill_ms": round(prefill_ms, 1),
         "decode_tokens_per_s": round(decode_tps, 1),
+        "observed_sclk_mhz": sclk.result(),
         "kernel_ms_per_rollout": per_step,
         "kept_fraction": kept_frac,
         "recompute": recompute,
