@@ -148,7 +148,8 @@ def gemm_flops(wl, rows: int) -> dict:
 
 def cpu_baseline(wl, weights, prompts, seconds: float) -> dict:
     """The oracle (float64 full recompute + float32 sampler) generating tokens for the
-    workload's first prompt until `seconds` have passed (at least one token)."""
+    workload's first prompt until `seconds` have passed (at least one token); then the
+    small fp32 configuration's whole rollout (16 sequences x 32 tokens) as `tiny_full`."""
     import dataclasses
 
     import numpy as np
@@ -169,6 +170,19 @@ def cpu_baseline(wl, weights, prompts, seconds: float) -> dict:
         if time.perf_counter() - t0 >= seconds:
             break
     dt = time.perf_counter() - t0
+    # and the small fp32 configuration in full: every sequence and token of its rollout
+    from paper_2505_17218_amd import synth
+
+    tw = synth.WORKLOADS["tiny"]
+    tsd, tww, tpr = dataclasses.asdict(tw.shape), synth.make_weights(tw.shape, 0), synth.make_prompts(tw, 0)
+    t1 = time.perf_counter()
+    for i in range(tw.n_seqs):
+        tseq = list(tpr[i // tw.group])
+        for t in range(tw.gen_len):
+            lg = om.forward(tsd, tww, np.array(tseq, dtype=np.int32), positions=[len(tseq) - 1])[0]
+            tok, _ = osm.sample_row(lg.astype(np.float32), i, t, tw.temperature, synth.sampler_seed(0))
+            tseq.append(tok)
+    tiny_dt = time.perf_counter() - t1
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     cpu_model = None
     try:
@@ -179,7 +193,9 @@ def cpu_baseline(wl, weights, prompts, seconds: float) -> dict:
     return {"value": n / dt, "unit": "generated tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{wl.shape.name} shape, 1 sequence, prompt {wl.prompt_len}, {n} tokens generated by "
                       f"full float64 recompute in {dt:.1f} s",
-            "cpu_model": cpu_model, "host_cpus_available": len(os.sched_getaffinity(0))}
+            "cpu_model": cpu_model, "host_cpus_available": len(os.sched_getaffinity(0)),
+            "tiny_full": {"workload": tw.name, "sequences": tw.n_seqs, "tokens": tw.n_seqs * tw.gen_len,
+                          "seconds": round(tiny_dt, 2), "tokens_per_s": round(tw.n_seqs * tw.gen_len / tiny_dt, 1)}}
 
 
 def kl_leg(shape, model, kv, seqs, P, adv, kept, lp_rollout, kept_l, N, T):
