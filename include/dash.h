@@ -157,7 +157,7 @@ size_t dash_kv_table_bytes(int32_t max_seqs, int32_t max_ctx, int32_t page_size)
  * (dash_kv_table_bytes).  Enqueues a clear of the page table on `stream`.
  * max_ctx bounds every slot's length (prompt + generated tokens).
  * Decode attention cuts a slot's context into splits whose length is fixed here
- * from max_seqs, the kv heads and max_ctx (long splits for large capacities,
+ * from max_seqs, the kv heads, the head dim and max_ctx (long splits for large capacities,
  * short ones so that small batches still fill the GPU); a sequence's results in
  * one cache therefore never depend on which other rows share its batch.
  */
