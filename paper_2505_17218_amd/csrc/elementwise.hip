@@ -139,6 +139,12 @@ __global__ void rope_table_k(const int32_t* __restrict__ pos, float* __restrict_
 }
 
 // grid (rows, ceil(items / 256)): one RoPE pair of q or k, or one v element, per thread.
+// KV-cache appends: non-temporal stores, as in the QKV GEMM's fused epilogue (a decode step
+// writes a few bytes into lines that later steps read from memory anyway).
+template <typename T> DASH_DEV void st_kv(T* p, float v);
+template <> DASH_DEV void st_kv<float>(float* p, float v) { __builtin_nontemporal_store(v, p); }
+template <> DASH_DEV void st_kv<bf16_t>(bf16_t* p, float v) { __builtin_nontemporal_store(f2bf(v), p); }
+
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads)
 qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride, const T* __restrict__ bias,
@@ -185,12 +191,12 @@ qkv_rope_append_k(const float* __restrict__ qkv, int nsplit, size_t split_stride
             st_elem(q + i + half, hi);
         } else if (page >= 0) {
             T* kb = pool + kv_block(g, layer, page, h - n_heads, 0);
-            st_elem(kb + k_index<T>(g, key, i), lo);
-            st_elem(kb + k_index<T>(g, key, i + half), hi);
+            st_kv(kb + k_index<T>(g, key, i), lo);
+            st_kv(kb + k_index<T>(g, key, i + half), hi);
         }
     } else if (is_v && page >= 0) {
         T* vb = pool + kv_block(g, layer, page, h, 1);
-        st_elem(vb + v_index<T>(g, key, i), a);
+        st_kv(vb + v_index<T>(g, key, i), a);
     }
 }
 

@@ -255,8 +255,9 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
                     q[i + half] = f2bf(hi);
                 } else if (row_page[rl] >= 0) {
                     bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) / hd, 0);
-                    kb[k_index_bf16(g, row_key[rl], i)] = f2bf(lo);
-                    kb[k_index_bf16(g, row_key[rl], i + half)] = f2bf(hi);
+                    // cache appends are non-temporal stores (see the v append below)
+                    __builtin_nontemporal_store(f2bf(lo), &kb[k_index_bf16(g, row_key[rl], i)]);
+                    __builtin_nontemporal_store(f2bf(hi), &kb[k_index_bf16(g, row_key[rl], i + half)]);
                 }
             }
         } else {
@@ -268,7 +269,11 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
                 if (m >= M || n >= N || row_page[rl] < 0) continue;
                 const float v = Cs[rl * CS + c] + bias_a;
                 bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
-                vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))] = f2bf(v);
+                // A decode step writes one key per row: 2 bytes into each of the 16-byte groups
+                // of 8 keys, lines that later steps read from memory anyway.  Non-temporal
+                // stores keep these partial lines out of L2: measured 8% less QKV time and 2%
+                // less decode-attention time at 1.5B, 1024 sequences.
+                __builtin_nontemporal_store(f2bf(v), &vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))]);
             }
         }
     } else if constexpr (EPI == EPI_STORE_F32) {
