@@ -259,8 +259,9 @@ def main() -> int:
                     help="first run a plain 1 GiB device-to-device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
-              "(the rollout is data-parallel over prompt groups; see DESIGN.md for how it shards)", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the rollout is "
+              "data-parallel over prompt groups, so each GPU would run its own share of the groups; "
+              "the multi-GPU launcher is not implemented)", file=sys.stderr)
         return 2
 
     import dataclasses
