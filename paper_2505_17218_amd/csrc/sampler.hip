@@ -1,11 +1,11 @@
 // Vocab-wide temperature sampling: Gumbel-max with counter-based Philox noise.
 //
-// One workgroup of 256 threads per row.  Thread t walks vocab entries in groups
-// of four (one Philox call yields the noise of four consecutive entries) with a
-// stride of 256 groups, so a wave reads 1 KB of logits per step, coalesced.
-// Each thread keeps its best (score, index) and an online (max, sum of exp) for
-// the log-normaliser; waves merge with xor shuffles, then LDS merges the four
-// waves.  Ties in the score go to the smaller vocab index.  Built with
+// One workgroup of kThreads (1024) threads per row.  Thread t walks vocab entries
+// in groups of four (one Philox call yields the noise of four consecutive
+// entries) with a stride of kThreads groups, so a wave reads 1 KB of logits per
+// step, coalesced.  Each thread keeps its best (score, index) and an online (max,
+// sum of exp) for the log-normaliser; waves merge with xor shuffles, then LDS
+// merges the sixteen waves in order.  Ties in the score go to the smaller vocab index.  Built with
 // -ffp-contract=off: see sampler_math.h.
 //
 // Screening.  The exact noise -ln(-ln u) (two correctly rounded divisions) is
@@ -208,7 +208,7 @@ __global__ void screen_check_k(unsigned* max_err_bits) {
 
 // Log-probability of a given token under softmax(logits) (temperature 1), one
 // workgroup per row, with sample_k's log-normaliser computed in sample_k's order
-// (entries in groups of four with a stride of 256 groups, wave xor tree, the four
+// (entries in groups of four with a stride of kThreads groups, wave xor tree, the
 // waves in order): on the same logits it returns sample_k's log-prob bit for bit.
 __global__ void __launch_bounds__(kThreads)
 logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ tokens,
@@ -260,8 +260,8 @@ logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const 
 }
 
 // KL divergence between the next-token distributions of two models, one
-// workgroup per row pair, with the samplers' entry walk (groups of four, stride
-// 256 groups).  Each side keeps, over its entries of nonzero probability (logit
+// workgroup of kKlThreads per row pair, walking entries in groups of four with a
+// stride of kKlThreads groups.  Each side keeps, over its entries of nonzero probability (logit
 // not -inf), a running maximum m, z = sum e^(x - m) and w = sum e^(x - m) (x - y)
 // with y the other side's logit: exponentials by the hardware, sums in fp64.  Then
 //   D_KL(p_x || p_y) = w_x / z_x - (m_x - m_y) - (ln z_x - ln z_y),
