@@ -322,6 +322,44 @@ def test_grouped_decode_bitexact_vs_per_row(shape, n_prompts, G, P, steps):
         np.testing.assert_array_equal(a, b)
 
 
+def test_decode_halves_on_two_streams_bitexact():
+    """Two halves of a batch decoded at the same time on two streams (separate workspaces,
+    disjoint slots, shared prompt pages) give the full batch's logits bit for bit, at contexts
+    that need several attention splits."""
+    shape = BF16_A
+    n_prompts, G, P, steps = 4, 4, 300, 3
+    w = synth.make_weights(shape, 6)
+    wl = synth.Workload("t", shape, n_prompts, G, P, steps + 1)
+    prompts = synth.make_prompts(wl, 6)
+    model = engine.Model(shape, w)
+    N, H = n_prompts * G, n_prompts * G // 2
+    kv = make_kv(model, 32, N, P + steps + 1)
+    assert kv.split_keys < P  # the combine pass runs
+    engine.prefill(model, kv, dev_i32(prompts), G, list(range(N)))
+    wsa, wsb = model.workspace(H, kv.max_ctx), model.workspace(N - H, kv.max_ctx)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    cur = torch.cuda.current_stream()
+    rng = np.random.default_rng(1)
+    for t in range(steps):
+        L.dash_kv_reserve(kv.handle, list(range(N)), P + t + 1, engine.stream_handle())
+        toks = dev_i32(rng.integers(0, shape.vocab, N))
+        slots = dev_i32(np.arange(N))
+        pos = dev_i32(np.full(N, P + t))
+        full = engine.decode_step(model, kv, toks, slots, pos)
+        la = torch.empty(H, shape.vocab, dtype=torch.float32, device="cuda")
+        lb = torch.empty(N - H, shape.vocab, dtype=torch.float32, device="cuda")
+        for st in (s1, s2):
+            st.wait_stream(cur)
+        # both halves rewrite this step's K/V with the values the full step wrote
+        with torch.cuda.stream(s1):
+            engine.decode_step(model, kv, toks[:H], slots[:H], pos[:H], wsa, la)
+        with torch.cuda.stream(s2):
+            engine.decode_step(model, kv, toks[H:], slots[H:], pos[H:], wsb, lb)
+        cur.wait_stream(s1)
+        cur.wait_stream(s2)
+        np.testing.assert_array_equal(torch.cat([la, lb]).cpu().numpy(), full.cpu().numpy())
+
+
 def test_rollout_driver_matches_stepwise_tiny():
     wl = synth.WORKLOADS["tiny"]
     w = synth.make_weights(wl.shape, 0)
