@@ -229,8 +229,7 @@ int dash_prefill(dash_model* model, dash_kv* kv, const int32_t* d_prompt_tokens,
  * Attention of row b covers positions 0..d_pos[b] of its slot.  Steps over
  * disjoint slots may run at the same time on different streams, each with its
  * own workspace and logits (with kernel timing off the call changes no host
- * state);
- * a row's logits do not depend on the other rows of its call.
+ * state); a row's logits do not depend on the other rows of its call.
  */
 int dash_decode_step(dash_model* model, dash_kv* kv, const int32_t* d_tokens, const int32_t* d_slots,
                      const int32_t* d_pos, int32_t n_rows, float* d_logits, void* d_ws, size_t ws_bytes,
