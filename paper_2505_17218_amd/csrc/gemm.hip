@@ -42,7 +42,7 @@ DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 // row (i / 4) * 8 + (l / 32) * 4 + i % 4, column l % 32.
 // LDS tiles are row-major with rows padded to 72 elements (fragment reads of 16
 // consecutive rows hit distinct banks); global loads fill full 128-byte rows.
-template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI, int WPOL = 0>
 __global__ void __launch_bounds__(64 * WGM * WGN)
 gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __restrict__ C, int M, int N, int K,
              int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride, QkvRopeArgs qa) {
@@ -122,7 +122,7 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
             ra[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsA, a_off[i] + kb, 0, 0));
 #pragma unroll
         for (int i = 0; i < B_CH; ++i)
-            rb[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsW, b_off[i] + kb, 0, 0));
+            rb[st][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsW, b_off[i] + kb, 0, WPOL));
     };
     auto store = [&](int st, int buf) {
 #pragma unroll
@@ -309,7 +309,7 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
     }
 }
 
-template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI, int WPOL = 0>
 hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int nsplit,
                      size_t split_stride, hipStream_t st, const QkvRopeArgs& qa = QkvRopeArgs{}) {
     const int m_tiles = (M + BM - 1) / BM;
@@ -325,7 +325,7 @@ hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, 
     // k-steps of 64 never straddle the end of K or of a split; byte offsets fit 31 bits
     if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
     const int blocks = m_tiles * n_tiles * nsplit;
-    gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI><<<blocks, 64 * WGM * WGN, 0, st>>>(
+    gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI, WPOL><<<blocks, 64 * WGM * WGN, 0, st>>>(
         (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride, qa);
     return hipGetLastError();
 }
@@ -426,6 +426,11 @@ hipError_t launch_gemm_qkv_rope(const void* A, const void* W, int M, int N, int 
     return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(A, W, nullptr, M, N, K, 0, 1, 0, st, qa);
 }
 
+// Cache policy of the weight loads where the batch fits one 64-row block: every
+// weight byte is then read by exactly one work-group, so the loads stream past the
+// caches (the same non-temporal policy as the decode attention's private K/V loads).
+constexpr int kWeightStream = 2;
+
 hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C, int M, int N, int K, int ldc,
                        int nsplit, size_t split_stride, hipStream_t st) {
     if (M <= 0 || N <= 0) return hipSuccess;
@@ -445,14 +450,17 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             // (d_ff >= 8192).  Measured on the 1.5B and 3B shapes: 9-11% faster up to 64
             // rows (three k-steps in flight), 5-16% at 129-256 rows, 3-5% slower at 65-128.
             if ((N / 2 + 63) / 64 >= 128) {
-                if (M <= 64) return run_bf16<64, 128, 2, 2, 3, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+                if (M <= 64)
+                    return run_bf16<64, 128, 2, 2, 3, EPI_SWIGLU, kWeightStream>(A, W, C, M, N, K, ldc, 1, 0, st);
                 if (M > 128) return run_bf16<64, 128, 2, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
             }
+            if (M <= 64) return run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU, kWeightStream>(A, W, C, M, N, K, ldc, 1, 0, st);
             return run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
         }
         if (N >= 8192) {  // LM head: many tiles, the largest tile that the batch fills wins
             if (M <= 64)
-                return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+                return run_bf16<64, 256, 1, 4, 2, EPI_STORE_F32, kWeightStream>(A, W, C, M, N, K, ldc, nsplit,
+                                                                               split_stride, st);
             if (M <= 128)  // measured 10-18% faster than 256x256 at 96-128 rows
                 return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
@@ -462,6 +470,9 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             // instead of two pull them faster while the launch is small (unsplit K, or one
             // 64-row block): measured 22-28% faster on the 1.5B and 3B QKV / O shapes up to
             // 256 rows and on the split down projection up to 64 rows.
+            if (M <= 64)
+                return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32, kWeightStream>(A, W, C, M, N, K, ldc, nsplit,
+                                                                              split_stride, st);
             return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
         // Larger batches: the largest tile that still gives the launch enough work-groups.
