@@ -16,6 +16,9 @@ the rollouts use:
   the policy-gradient loss over the kept samples (Sec. 3.2, Eq. (2)).
 * :mod:`oracle.policy`    — the KL regulariser D_KL(pi_base || pi_theta) and the
   clipped PPO surrogate with sequence ratios (Sec. 3.2), float64.
+* :mod:`oracle.rollout`   — a whole preemptive-sampling rollout with per-sample
+  completion lengths (Sec. 3.4, App. A maximum completion length): the live-row
+  schedule, row compaction, page accounting of the group fork, and the tokens.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP path

@@ -26,7 +26,10 @@ torch.nn.functional (rms_norm, scaled_dot_product_attention, silu, linear) with
 RoPE written as complex multiplication; scalar-loop brute force on a micro
 shape; the one-token closed form (attention over a single key returns its
 value); RoPE identity at position 0, norm preservation and relative-position
-invariance; and causality (logits at position i do not depend on later tokens).
+invariance; causality (logits at position i do not depend on later tokens); and,
+for the bfloat16 storage points, a scalar-loop brute force that rounds with
+torch's own bfloat16 conversion at exactly those points (equal to the oracle,
+while leaving out any single point moves the logits visibly).
 """
 from __future__ import annotations
 

@@ -57,9 +57,11 @@ def _torch_reference(shape: dict, weights: dict, tokens: np.ndarray) -> np.ndarr
     return F.linear(y, E).numpy()
 
 
-def _brute(shape: dict, weights: dict, tokens) -> np.ndarray:
-    """Scalar loops over every index (micro shapes only)."""
+def _brute(shape: dict, weights: dict, tokens, rnd=None) -> np.ndarray:
+    """Scalar loops over every index (micro shapes only).  ``rnd(point, values)``, if given,
+    is applied to the list of values at each named storage point (see BF16_POINTS)."""
     W = {k: om.as_f64(v) for k, v in weights.items()}
+    R = rnd or (lambda point, vals: vals)
     L, Hq, Hkv, hd = shape["n_layers"], shape["n_heads"], shape["n_kv_heads"], shape["head_dim"]
     ff, eps, d, V = shape["d_ff"], shape["rms_eps"], shape["d_model"], shape["vocab"]
     S = len(tokens)
@@ -88,10 +90,10 @@ def _brute(shape: dict, weights: dict, tokens) -> np.ndarray:
         p = f"l{l}."
         qs, ks, vs = [], [], []
         for s in range(S):
-            qkv = lin(norm(x[s], W[p + "attn_norm"]), W[p + "w_qkv"], W[p + "b_qkv"])
-            qs.append([rot(qkv[h * hd:(h + 1) * hd], s) for h in range(Hq)])
-            ks.append([rot(qkv[(Hq + h) * hd:(Hq + h + 1) * hd], s) for h in range(Hkv)])
-            vs.append([qkv[(Hq + Hkv + h) * hd:(Hq + Hkv + h + 1) * hd] for h in range(Hkv)])
+            qkv = lin(R("attn_in", norm(x[s], W[p + "attn_norm"])), W[p + "w_qkv"], W[p + "b_qkv"])
+            qs.append([R("q", rot(qkv[h * hd:(h + 1) * hd], s)) for h in range(Hq)])
+            ks.append([R("k", rot(qkv[(Hq + h) * hd:(Hq + h + 1) * hd], s)) for h in range(Hkv)])
+            vs.append([R("v", qkv[(Hq + Hkv + h) * hd:(Hq + Hkv + h + 1) * hd]) for h in range(Hkv)])
         for s in range(S):
             o = []
             for h in range(Hq):
@@ -101,12 +103,12 @@ def _brute(shape: dict, weights: dict, tokens) -> np.ndarray:
                 e = [math.exp(a - m) for a in sc]
                 z = sum(e)
                 o += [sum(e[j] / z * vs[j][g][i] for j in range(s + 1)) for i in range(hd)]
-            x[s] = [a + b for a, b in zip(x[s], lin(o, W[p + "w_o"]))]
+            x[s] = [a + b for a, b in zip(x[s], lin(R("attn_out", o), W[p + "w_o"]))]
         for s in range(S):
-            gu = lin(norm(x[s], W[p + "mlp_norm"]), W[p + "w_gate_up"])
+            gu = lin(R("mlp_in", norm(x[s], W[p + "mlp_norm"])), W[p + "w_gate_up"])
             hh = [gu[i] / (1.0 + math.exp(-gu[i])) * gu[ff + i] for i in range(ff)]
-            x[s] = [a + b for a, b in zip(x[s], lin(hh, W[p + "w_down"]))]
-    return np.array([lin(norm(x[s], W["final_norm"]), W["embed"]) for s in range(S)])
+            x[s] = [a + b for a, b in zip(x[s], lin(R("swiglu", hh), W[p + "w_down"]))]
+    return np.array([lin(R("final_in", norm(x[s], W["final_norm"])), W["embed"]) for s in range(S)])
 
 
 @pytest.fixture(scope="module")
@@ -158,6 +160,52 @@ def test_bf16_shape_matches_reference_up_to_rounding_points():
     got = om.forward(shape, w, toks)
     err = np.abs(got - ref).max()
     assert 1e-5 < err < 2e-2, err
+
+
+# Storage points where the bfloat16 path keeps bfloat16 values: the normalised input of the
+# QKV projection, q and k after RoPE, v (the cached keys and values), the attention output
+# (left operand of the output projection), the normalised MLP input, the SwiGLU product
+# (left operand of the down projection) and the normalised input of the LM head.
+BF16_POINTS = ("attn_in", "q", "k", "v", "attn_out", "mlp_in", "swiglu", "final_in")
+MICRO_BF16 = synth.Shape("micro-bf16", 2, 8, 4, 2, 4, 12, 16, 10000.0, synth.DT_BF16)
+
+
+def _torch_bf16(vals):
+    """Nearest bfloat16 by torch's own conversion (a library routine, not the oracle's bit trick)."""
+    return torch.tensor(vals, dtype=torch.float64).to(torch.bfloat16).to(torch.float64).tolist()
+
+
+@pytest.fixture(scope="module")
+def micro_bf16():
+    w = synth.make_weights(MICRO_BF16, seed=4)
+    rng = np.random.default_rng(12)
+    for k in w:
+        if k.endswith("norm"):
+            v = (1.0 + 0.5 * rng.standard_normal(w[k].shape)).astype(np.float32)
+        elif w[k].size:
+            v = (om.as_f64(w[k]) * 25).astype(np.float32)  # O(0.5) weights
+        else:
+            continue
+        w[k] = synth._to_bf16_bits(v)
+    return _shape(MICRO_BF16), w
+
+
+def test_bf16_rounding_points_pinned_by_brute_force(micro_bf16):
+    """The bfloat16 oracle equals a scalar-loop brute force that rounds (with torch's
+    conversion) at exactly the eight storage points; leaving out any one of them moves the
+    logits by far more than the agreement, so a missing, extra or misplaced rounding point
+    in the oracle fails here."""
+    shape, w = micro_bf16
+    toks = [3, 1, 4, 1, 5, 9, 2, 6, 5, 3]
+    got = om.forward(shape, w, np.array(toks, dtype=np.int32))
+    full = _brute(shape, w, toks, rnd=lambda point, vals: _torch_bf16(vals))
+    np.testing.assert_allclose(got, full, rtol=1e-9, atol=1e-9)
+    for skip in BF16_POINTS:
+        part = _brute(shape, w, toks, rnd=lambda point, vals, skip=skip: vals if point == skip else _torch_bf16(vals))
+        assert np.abs(part - got).max() > 1e-3, skip
+    # and the float32 network (no rounding at all) is the dtype-0 oracle on the same weights
+    np.testing.assert_allclose(om.forward(dict(shape, dtype=0), w, np.array(toks, dtype=np.int32)),
+                               _brute(shape, w, toks), rtol=1e-10, atol=1e-10)
 
 
 def test_causal_prefix_consistency(micro):
