@@ -18,6 +18,7 @@
 #include "../../include/dash.h"
 #include "common.h"
 #include "kernels.h"
+#include "kv_pages.h"
 
 using namespace dash;
 
@@ -207,11 +208,7 @@ struct dash_kv {
     uint32_t* d_status;
     KVGeom g;
     int max_ctx;
-    std::vector<int32_t> table;   // [max_seqs][max_pages], -1 = none
-    std::vector<int32_t> len;     // per slot
-    std::vector<int32_t> npages;  // pages mapped per slot
-    std::vector<int32_t> refc;    // per page
-    std::vector<int32_t> free_list;
+    PageBook pb;  // host mirror of the page table, reference counts, free list
     // pinned staging ring for uploads (two halves, each guarded by an event)
     char* stage = nullptr;
     size_t stage_half = 0;
@@ -253,30 +250,23 @@ int kv_upload(dash_kv* kv, void* dst, const void* src, size_t bytes, hipStream_t
 int kv_push_rows(dash_kv* kv, int s0, int s1, hipStream_t st) {
     if (s1 < s0) return DASH_OK;
     const size_t mp = kv->g.max_pages;
-    return kv_upload(kv, kv->d_table + s0 * mp, kv->table.data() + s0 * mp, (size_t)(s1 - s0 + 1) * mp * 4, st);
+    return kv_upload(kv, kv->d_table + s0 * mp, kv->pb.table.data() + s0 * mp, (size_t)(s1 - s0 + 1) * mp * 4, st);
 }
 
-int kv_alloc_page(dash_kv* kv) {
-    const int p = kv->free_list.back();
-    kv->free_list.pop_back();
-    kv->refc[p] = 1;
-    return p;
-}
-
-void kv_unref(dash_kv* kv, int p) {
-    if (--kv->refc[p] == 0) kv->free_list.push_back(p);
-}
-
-// Map pages so that positions [0, new_len) of `slot` are backed (host mirror only;
-// the caller uploads the rows).  The caller has checked that enough pages are free.
-void kv_grow(dash_kv* kv, int slot, int new_len) {
-    const int want = (new_len + kv->g.page_size - 1) / kv->g.page_size;
-    while (kv->npages[slot] < want) {
-        kv->table[(size_t)slot * kv->g.max_pages + kv->npages[slot]] = kv_alloc_page(kv);
-        kv->npages[slot]++;
+// Returns the listed slots' pages to the pool unless disarmed: a call that fails
+// after mapping pages (a failed launch) leaves the cache as it found it.  Work
+// already enqueued may still write those pages; they are reused only by later
+// stream-ordered work.
+struct ReleaseOnError {
+    dash_kv* kv;
+    const int32_t* slots;
+    int n;
+    bool armed = true;
+    ~ReleaseOnError() {
+        if (armed)
+            for (int i = 0; i < n; ++i) kv->pb.release(slots[i]);
     }
-    kv->len[slot] = std::max(kv->len[slot], new_len);
-}
+};
 
 }  // namespace
 
@@ -433,12 +423,7 @@ int dash_kv_create(const dash_model* m, void* pool, size_t pool_bytes, int32_t p
     const size_t ent = table_entries(max_seqs, max_ctx, ps);
     kv->d_table = (int32_t*)d_table;
     kv->d_status = (uint32_t*)((char*)d_table + align_up(ent * 4, 256));
-    kv->table.assign(ent, -1);
-    kv->len.assign(max_seqs, 0);
-    kv->npages.assign(max_seqs, 0);
-    kv->refc.assign(pages, 0);
-    kv->free_list.resize(pages);
-    for (size_t i = 0; i < pages; ++i) kv->free_list[i] = (int32_t)(pages - 1 - i);  // pop_back gives 0, 1, 2...
+    kv->pb.init((int)pages, max_seqs, max_pages, ps);
     kv->stage_half = std::max<size_t>(align_up(ent * 4, 256), 1 << 16);
     hipError_t e = hipHostMalloc((void**)&kv->stage, 2 * kv->stage_half, hipHostMallocDefault);
     if (e != hipSuccess) {
@@ -480,14 +465,14 @@ void dash_kv_destroy(dash_kv* kv) {
 
 int dash_kv_free_pages(const dash_kv* kv, int32_t* out) {
     if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
-    *out = (int32_t)kv->free_list.size();
+    *out = (int32_t)kv->pb.free_pages();
     return DASH_OK;
 }
 
 int dash_kv_slot_len(const dash_kv* kv, int32_t slot, int32_t* out) {
     if (!kv || !out) return fail(DASH_EINVAL, "NULL argument");
     if (slot < 0 || slot >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", slot);
-    *out = kv->len[slot];
+    *out = kv->pb.len[slot];
     return DASH_OK;
 }
 
@@ -501,24 +486,18 @@ int dash_kv_reserve(dash_kv* kv, const int32_t* h_slots, int32_t n, int32_t new_
     if (!kv || (n > 0 && !h_slots)) return fail(DASH_EINVAL, "NULL argument");
     if (n < 0 || new_len < 0) return fail(DASH_EINVAL, "negative count or length");
     if (new_len > kv->max_ctx) return fail(DASH_ECAPACITY, "new_len %d exceeds max_ctx %d", new_len, kv->max_ctx);
-    const int ps = kv->g.page_size, mp = kv->g.max_pages;
-    size_t need = 0;
     for (int i = 0; i < n; ++i) {
         const int s = h_slots[i];
         if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
-        const int want = (new_len + ps - 1) / ps;
-        if (want > kv->npages[s]) need += want - kv->npages[s];
     }
     // duplicates in h_slots would double count: harmless (over-estimate)
-    if (need > kv->free_list.size())
-        return fail(DASH_ECAPACITY, "pool exhausted: need %zu pages, %zu free", need, kv->free_list.size());
-    (void)mp;
+    const size_t need = kv->pb.grow_need(h_slots, n, new_len);
+    if (need > kv->pb.free_pages())
+        return fail(DASH_ECAPACITY, "pool exhausted: need %zu pages, %zu free", need, kv->pb.free_pages());
     int lo = kv->g.max_seqs, hi = -1;
     for (int i = 0; i < n; ++i) {
         const int s = h_slots[i];
-        const int before = kv->npages[s];
-        kv_grow(kv, s, new_len);
-        if (kv->npages[s] != before) {
+        if (kv->pb.grow(s, new_len)) {
             lo = std::min(lo, s);
             hi = std::max(hi, s);
         }
@@ -528,17 +507,11 @@ int dash_kv_reserve(dash_kv* kv, const int32_t* h_slots, int32_t n, int32_t new_
 
 int dash_kv_release(dash_kv* kv, const int32_t* h_slots, int32_t n) {
     if (!kv || (n > 0 && !h_slots)) return fail(DASH_EINVAL, "NULL argument");
-    const int mp = kv->g.max_pages;
     for (int i = 0; i < n; ++i) {
         const int s = h_slots[i];
         if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
-        for (int j = 0; j < kv->npages[s]; ++j) {
-            kv_unref(kv, kv->table[(size_t)s * mp + j]);
-            kv->table[(size_t)s * mp + j] = -1;
-        }
-        kv->npages[s] = 0;
-        kv->len[s] = 0;
     }
+    for (int i = 0; i < n; ++i) kv->pb.release(h_slots[i]);
     // The device rows keep stale page ids until the slot is reused (the next
     // reserve / prefill of the slot uploads its row); nothing reads a released slot.
     return DASH_OK;
@@ -603,8 +576,18 @@ int dash_profile_read(double* ms_out, int64_t* launches_out, int32_t reset) {
 
 namespace {
 
+// Most token rows one forward pass may hold: the bf16 GEMMs address their left
+// operand [rows, K] with 32-bit byte offsets, so rows * K * 2 must stay below 2^31
+// for every K of the layer (d_model, the attention width and d_ff).
+int max_forward_rows(const dash_model* m) {
+    const int64_t k = std::max({(int64_t)m->d.d_model, (int64_t)m->d.n_heads * m->d.head_dim, (int64_t)m->d.d_ff});
+    return (int)std::min<int64_t>(((int64_t)1 << 31) / (2 * k) - 1, 0x7FFFFFFF);
+}
+
 int ws_rows_for(const dash_model* m, size_t ws_bytes, int want) {
-    // largest row count <= want whose plan fits (plans grow monotonically in rows)
+    // largest row count <= want (and <= max_forward_rows) whose plan fits (plans grow
+    // monotonically in rows)
+    want = std::min(want, max_forward_rows(m));
     if (plan_ws(m, want, nullptr, 0).bytes <= ws_bytes) return want;
     int lo = 0, hi = want;
     while (lo < hi) {
@@ -712,6 +695,8 @@ int run_layers(dash_model* m, dash_kv* kv, const Ws& w, int rows, const int32_t*
 }
 
 int check_ws(const dash_model* m, void* ws, size_t ws_bytes, int rows, int max_ctx) {
+    if (rows > max_forward_rows(m))
+        return fail(DASH_ENOTSUP, "%d rows exceed the %d one forward pass may hold", rows, max_forward_rows(m));
     if (!ws) return fail(DASH_EINVAL, "workspace is NULL");
     if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
     const size_t need = plan_ws(m, rows, nullptr, max_ctx).bytes;
@@ -744,41 +729,21 @@ int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
 int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prompts, int P, int G,
                  const int32_t* h_slots, float* d_logits, void* ws, size_t ws_bytes, hipStream_t st) {
     const auto& d = m->d;
-    const int ps = kv->g.page_size, mp = kv->g.max_pages;
     // capacity: full prompt pages once per prompt, one private partial page per sample
-    const int full = P / ps, part = P % ps ? 1 : 0;
-    const size_t need = (size_t)n_prompts * (full + (size_t)part * G);
-    if (need > kv->free_list.size())
-        return fail(DASH_ECAPACITY, "pool exhausted: prefill needs %zu pages, %zu free", need, kv->free_list.size());
-    const int rows_fit = ws_rows_for(m, ws_bytes, n_prompts * P);
+    const size_t need = kv->pb.fork_need(n_prompts, P, G);
+    if (need > kv->pb.free_pages())
+        return fail(DASH_ECAPACITY, "pool exhausted: prefill needs %zu pages, %zu free", need, kv->pb.free_pages());
+    const int rows_fit = ws_rows_for(m, ws_bytes, (int)std::min<int64_t>((int64_t)n_prompts * P, 0x7FFFFFFF));
     int chunk = rows_fit / P;
-    if (chunk < 1) return fail(DASH_ECAPACITY, "workspace cannot hold one prompt of %d tokens", P);
+    if (chunk < 1)
+        return fail(P > max_forward_rows(m) ? DASH_ENOTSUP : DASH_ECAPACITY,
+                    "workspace cannot hold one prompt of %d tokens", P);
     const int n_chunks = (n_prompts + chunk - 1) / chunk;
     chunk = (n_prompts + n_chunks - 1) / n_chunks;  // as many chunks, of equal size (the last may be smaller)
     // host bookkeeping: pages of every sample's slot
     std::vector<int32_t> pairs;
-    for (int p = 0; p < n_prompts; ++p) {
-        const int s0 = h_slots[p * G];
-        for (int j = 0; j < full + part; ++j) kv->table[(size_t)s0 * mp + j] = kv_alloc_page(kv);
-        kv->npages[s0] = full + part;
-        kv->len[s0] = P;
-        for (int g = 1; g < G; ++g) {
-            const int s = h_slots[p * G + g];
-            for (int j = 0; j < full; ++j) {
-                const int pg = kv->table[(size_t)s0 * mp + j];
-                kv->table[(size_t)s * mp + j] = pg;
-                kv->refc[pg]++;
-            }
-            if (part) {
-                const int pg = kv_alloc_page(kv);
-                kv->table[(size_t)s * mp + full] = pg;
-                pairs.push_back(kv->table[(size_t)s0 * mp + full]);
-                pairs.push_back(pg);
-            }
-            kv->npages[s] = full + part;
-            kv->len[s] = P;
-        }
-    }
+    kv->pb.fork(h_slots, n_prompts, P, G, pairs);
+    ReleaseOnError guard{kv, h_slots, n_prompts * G};
     int lo = kv->g.max_seqs, hi = -1;
     for (int i = 0; i < n_prompts * G; ++i) {
         lo = std::min(lo, h_slots[i]);
@@ -818,6 +783,7 @@ int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prom
             DASH_HIP(launch_copy_pages(d.dtype, kv->pool, kv->g, w.pairs, c, st));
         }
     }
+    guard.armed = false;
     return DASH_OK;
 }
 
@@ -838,7 +804,7 @@ int dash_prefill(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int32_t n_
         if (s < 0 || s >= kv->g.max_seqs) return fail(DASH_EINVAL, "slot %d out of range", s);
         if (seen[s]) return fail(DASH_EINVAL, "slot %d listed twice", s);
         seen[s] = 1;
-        if (kv->npages[s] || kv->len[s]) return fail(DASH_EINVAL, "slot %d is not empty", s);
+        if (!kv->pb.empty(s)) return fail(DASH_EINVAL, "slot %d is not empty", s);
     }
     if (!ws) return fail(DASH_EINVAL, "workspace is NULL");
     if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
@@ -1047,13 +1013,15 @@ int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_to
     if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
     const hipStream_t st = (hipStream_t)stream;
     const auto& d = m->d;
-    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    const int ps = kv->g.page_size;
     const int pps = (L + ps - 1) / ps;  // private pages per sequence
     const int Tg = L - P;
     // chunk: the most sequences that fit the workspace, the slots and the free pages
     int cmax = std::min<int>(n_seqs, kv->g.max_seqs);
-    cmax = std::min<int>(cmax, (int)(kv->free_list.size() / pps));
+    cmax = std::min<int>(cmax, (int)(kv->pb.free_pages() / pps));
     if (cmax < 1) return fail(DASH_ECAPACITY, "the pool cannot hold one sequence of %d tokens", L);
+    cmax = std::min(cmax, max_forward_rows(m) / L);  // every row of a chunk goes through the GEMMs
+    if (cmax < 1) return fail(DASH_ENOTSUP, "seq_len %d exceeds the rows one forward pass may hold", L);
     int lo = 0, hi = cmax;
     while (lo < hi) {
         const int mid = (lo + hi + 1) / 2;
@@ -1065,7 +1033,7 @@ int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_to
         return fail(DASH_ECAPACITY, "workspace too small: %zu < %zu bytes for one sequence", ws_bytes,
                     plan_tf(m, 1, L, P, nullptr).bytes);
     for (int j = 0; j < c; ++j)
-        if (kv->npages[j] || kv->len[j]) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
+        if (!kv->pb.empty(j)) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
     const TfWs t = plan_tf(m, c, L, P, (char*)ws);
     const Ws& w = t.step;
     std::vector<int32_t> pos, slot, gather, slots(c);
@@ -1073,11 +1041,8 @@ int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_to
     int rc;
     for (int s0 = 0; s0 < n_seqs; s0 += c) {
         const int nc = std::min(c, n_seqs - s0);
-        for (int j = 0; j < nc; ++j) {
-            for (int p = 0; p < pps; ++p) kv->table[(size_t)j * mp + p] = kv_alloc_page(kv);
-            kv->npages[j] = pps;
-            kv->len[j] = L;
-        }
+        for (int j = 0; j < nc; ++j) kv->pb.grow(j, L);
+        ReleaseOnError guard{kv, slots.data(), nc};
         if ((rc = kv_push_rows(kv, 0, nc - 1, st))) return rc;
         const int rows = nc * L, rows_lm = nc * Tg;
         pos.resize(rows);
@@ -1094,6 +1059,7 @@ int dash_teacher_forced_logprobs(dash_model* m, dash_kv* kv, const int32_t* d_to
         const int32_t* tok = d_tokens + (size_t)s0 * L;
         if ((rc = tf_forward(m, kv, w, tok, rows, rows_lm, L, t.logits, st))) return rc;
         DASH_HIP(launch_logprob_gather(t.logits, d.vocab, rows_lm, d.vocab, tok, Tg, L, P, d_lp + (size_t)s0 * Tg, st));
+        guard.armed = false;
         if ((rc = dash_kv_release(kv, slots.data(), nc))) return rc;
     }
     return DASH_OK;
@@ -1148,12 +1114,14 @@ int dash_teacher_forced_kl(dash_model* m, dash_model* base, dash_kv* kv, const i
     if ((uintptr_t)ws & 255) return fail(DASH_EINVAL, "workspace must be 256-byte aligned");
     const hipStream_t st = (hipStream_t)stream;
     const auto& d = m->d;
-    const int ps = kv->g.page_size, mp = kv->g.max_pages;
+    const int ps = kv->g.page_size;
     const int pps = (L + ps - 1) / ps;
     const int Tg = L - P;
     int cmax = std::min<int>(n_seqs, kv->g.max_seqs);
-    cmax = std::min<int>(cmax, (int)(kv->free_list.size() / pps));
+    cmax = std::min<int>(cmax, (int)(kv->pb.free_pages() / pps));
     if (cmax < 1) return fail(DASH_ECAPACITY, "the pool cannot hold one sequence of %d tokens", L);
+    cmax = std::min(cmax, max_forward_rows(m) / L);
+    if (cmax < 1) return fail(DASH_ENOTSUP, "seq_len %d exceeds the rows one forward pass may hold", L);
     int lo = 0, hi = cmax;
     while (lo < hi) {
         const int mid = (lo + hi + 1) / 2;
@@ -1165,7 +1133,7 @@ int dash_teacher_forced_kl(dash_model* m, dash_model* base, dash_kv* kv, const i
         return fail(DASH_ECAPACITY, "workspace too small: %zu < %zu bytes for one sequence", ws_bytes,
                     plan_tf_kl(m, 1, L, P, nullptr).bytes);
     for (int j = 0; j < c; ++j)
-        if (kv->npages[j] || kv->len[j]) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
+        if (!kv->pb.empty(j)) return fail(DASH_EINVAL, "kv slot %d is not empty", j);
     const TfKlWs t = plan_tf_kl(m, c, L, P, (char*)ws);
     const Ws& w = t.step;
     std::vector<int32_t> pos, slot, gather, slots(c);
@@ -1173,11 +1141,8 @@ int dash_teacher_forced_kl(dash_model* m, dash_model* base, dash_kv* kv, const i
     int rc;
     for (int s0 = 0; s0 < n_seqs; s0 += c) {
         const int nc = std::min(c, n_seqs - s0);
-        for (int j = 0; j < nc; ++j) {
-            for (int p = 0; p < pps; ++p) kv->table[(size_t)j * mp + p] = kv_alloc_page(kv);
-            kv->npages[j] = pps;
-            kv->len[j] = L;
-        }
+        for (int j = 0; j < nc; ++j) kv->pb.grow(j, L);
+        ReleaseOnError guard{kv, slots.data(), nc};
         if ((rc = kv_push_rows(kv, 0, nc - 1, st))) return rc;
         const int rows = nc * L, rows_lm = nc * Tg;
         pos.resize(rows);
@@ -1200,6 +1165,7 @@ int dash_teacher_forced_kl(dash_model* m, dash_model* base, dash_kv* kv, const i
                                            st));
         DASH_HIP(launch_logits_kl(t.logits, t.logits_base, d.vocab, rows_lm, d.vocab, d_kl + (size_t)s0 * Tg,
                                   d_kl_rev ? d_kl_rev + (size_t)s0 * Tg : nullptr, st));
+        guard.armed = false;
         if ((rc = dash_kv_release(kv, slots.data(), nc))) return rc;
     }
     return DASH_OK;
@@ -1217,11 +1183,13 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
     if (n_prompts < 1 || P < 1 || G < 1 || T < 1) return fail(DASH_EINVAL, "sizes must be >= 1");
     if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DASH_EINVAL, "temperature must be > 0 and finite");
+    if ((int64_t)n_prompts * G > kv->g.max_seqs)
+        return fail(DASH_ECAPACITY, "kv has %d slots, rollout needs %lld", kv->g.max_seqs, (long long)n_prompts * G);
     const int N = n_prompts * G;
-    if (N > kv->g.max_seqs) return fail(DASH_ECAPACITY, "kv has %d slots, rollout needs %d", kv->g.max_seqs, N);
+    if (N > max_forward_rows(m)) return fail(DASH_ENOTSUP, "%d rows exceed the rows one forward pass may hold", N);
     if (P + T > kv->max_ctx) return fail(DASH_ECAPACITY, "prompt_len + gen_len exceeds max_ctx");
     for (int s = 0; s < N; ++s)
-        if (kv->npages[s] || kv->len[s]) return fail(DASH_EINVAL, "kv slot %d is not empty", s);
+        if (!kv->pb.empty(s)) return fail(DASH_EINVAL, "kv slot %d is not empty", s);
     std::vector<int32_t> budget(N, T);
     if (h_budget)
         for (int i = 0; i < N; ++i) {
@@ -1236,9 +1204,9 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
         const int ps = kv->g.page_size;
         size_t need = (size_t)n_prompts * (P / ps);
         for (int i = 0; i < N; ++i) need += (size_t)(P + budget[i] + ps - 1) / ps - P / ps;
-        if (need > kv->free_list.size())
+        if (need > kv->pb.free_pages())
             return fail(DASH_ECAPACITY, "pool too small for this rollout: %zu pages needed, %zu free", need,
-                        kv->free_list.size());
+                        kv->pb.free_pages());
     }
     hipStream_t st = (hipStream_t)stream;
     const auto& d = m->d;
@@ -1356,7 +1324,7 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
                 if (budget[i] > t) live_slots.push_back(i);
             // one page ahead, capped at the last position the sample will feed (P + budget - 2)
             const int ahead = (need_len + kv->g.page_size - 1) / kv->g.page_size * kv->g.page_size;
-            for (int s : live_slots) kv_grow(kv, s, std::min(P + budget[s] - 1, ahead));
+            for (int s : live_slots) kv->pb.grow(s, std::min(P + budget[s] - 1, ahead));
             if ((rc = kv_push_rows(kv, live_slots.front(), live_slots.back(), st))) {
                 destroy_graphs();
                 return rc;
@@ -1385,7 +1353,7 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     // release whatever is still held (fixed-length rollouts end with every slot live)
     std::vector<int32_t> held;
     for (int i = 0; i < N; ++i)
-        if (kv->npages[i]) held.push_back(i);
+        if (kv->pb.npages[i]) held.push_back(i);
     return dash_kv_release(kv, held.data(), (int)held.size());
 }
 
