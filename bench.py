@@ -241,6 +241,103 @@ def kl_leg(shape, model, kv, seqs, P, adv, kept, lp_rollout, kept_l, N, T):
     return out
 
 
+def workload_leg(wl, model, weights_seed: int = 0, kv_pages_extra: int = 8, budgets=None) -> dict:
+    """One rollout of `wl` on an already created model: a short warm-up rollout (8 tokens,
+    same batch) that loads the kernels, then one timed rollout of the full workload with the
+    middle decoder layer's decode attention timed by events, and the advantage filter of
+    the workload's rewards.  Returns tokens/s and the attention HBM fraction."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from paper_2505_17218_amd import _lib as L
+    from paper_2505_17218_amd import engine, synth
+
+    s = wl.shape
+    N, P, G, T = wl.n_seqs, wl.prompt_len, wl.group, wl.gen_len
+    ps = 32
+    if budgets is not None:
+        pages = wl.n_prompts * (P // ps) + int(sum((P + int(b) + ps - 1) // ps - P // ps for b in budgets))
+    else:
+        pages = wl.n_prompts * (P // ps) + N * ((P + T + ps - 1) // ps - P // ps)
+    kv = engine.KVCache(model, ps, N, P + T, pages + kv_pages_extra)
+    prompts = torch.from_numpy(synth.make_prompts(wl, weights_seed)).cuda()
+    rewards = torch.from_numpy(synth.make_rewards(wl.n_prompts, G, wl.reward, weights_seed)).cuda()
+    seed = synth.sampler_seed(weights_seed)
+    warm = engine.Rollout(model, kv, wl.n_prompts, P, G, 8)
+    warm.run(prompts, wl.temperature, seed, budgets=None if budgets is None else np.minimum(budgets, 8),
+             use_graph=budgets is None)
+    torch.cuda.synchronize()
+    del warm
+    ro = engine.Rollout(model, kv, wl.n_prompts, P, G, T)
+    layer = s.n_layers // 2
+    L.dash_profile_read(reset=True)
+    L.dash_profile_enable((1 << L.K["attn"]) | (1 << L.K["prefill"]))
+    L.dash_profile_layer(layer)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ro.run(prompts, wl.temperature, seed, budgets=budgets, use_graph=budgets is None)
+    _, kept = engine.advantage_filter(rewards, G, L.DASH_ADV_STD_SAMPLE, 1e-6, wl.tau)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = L.dash_profile_read(reset=True)
+    L.dash_profile_enable(0)
+    L.dash_profile_layer(-1)
+    gen = int(budgets.sum()) if budgets is not None else N * T
+    out = {"workload": wl.name, "sequences": N, "prompt_len": P, "gen_len": T, "ragged": budgets is not None,
+           "tokens": gen, "seconds": round(dt, 3), "tokens_per_s": round(gen / dt, 1),
+           "prefill_ms": round(prof["prefill"][0], 1), "kept_fraction": kept.numel() / N,
+           "attn_split_keys": kv.split_keys}
+    attn_ms, attn_n = prof["attn"]
+    if budgets is None and attn_n:
+        uniq, _ = attention_bytes(wl, T)
+        per_layer = uniq / s.n_layers
+        achieved = per_layer / (attn_ms * 1e-3) / 1e9
+        out["decode_attn"] = {"avg_launch_us": round(attn_ms / attn_n * 1e3, 2), "GBs": round(achieved, 1),
+                              "frac_hbm": round(achieved / HBM_PEAK_GBS, 4)}
+    del ro, kv
+    torch.cuda.empty_cache()
+    return out
+
+
+def legs(main_model, main_wl, max_seconds: float) -> dict:
+    """Compact legs over the other workloads, each timed once after a short warm-up: the 3B
+    batch sweep (64, 256, 1024, 2048 sequences), the 0.5B workload, and the ragged 1.5B
+    workload (its kept fraction reported).  Stops early once `max_seconds` have passed."""
+    import torch
+
+    from paper_2505_17218_amd import engine, synth
+
+    t0 = time.perf_counter()
+    out = {}
+
+    def left():
+        return max_seconds - (time.perf_counter() - t0)
+
+    rw = synth.WORKLOADS["1.5b-ragged"]
+    if main_wl.shape == rw.shape:
+        budgets = synth.make_lengths(rw.n_seqs, rw.ragged_mean, rw.gen_len, 0)
+        out[rw.name] = workload_leg(rw, main_model, budgets=budgets)
+        log(f"leg {rw.name}: {out[rw.name]}")
+    model = None
+    for name in ("0.5b-b512", "3b-b64", "3b-b256", "3b-b1024", "3b-b2048"):
+        if left() <= 0:
+            out[name] = "skipped (time budget)"
+            continue
+        wl = synth.WORKLOADS[name]
+        if model is None or model.shape != wl.shape:
+            model = None
+            torch.cuda.empty_cache()
+            model = engine.Model(wl.shape, synth.make_weights(wl.shape, 0))
+        out[name] = workload_leg(wl, model)
+        log(f"leg {name}: {out[name]}")
+    model = None
+    torch.cuda.empty_cache()
+    out["seconds"] = round(time.perf_counter() - t0, 1)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -255,6 +352,10 @@ def main() -> int:
                     help="skip the KL regulariser leg (teacher-forced KL against a second model, PPO loss)")
     ap.add_argument("--no-recompute", action="store_true",
                     help="skip the teacher-forced log-prob recompute of the kept samples after the timed region")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the compact legs over the other workloads (3B batch sweep, 0.5B, ragged 1.5B)")
+    ap.add_argument("--legs-seconds", type=float, default=240.0,
+                    help="stop starting new legs after this many seconds")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 1 GiB device-to-device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
@@ -413,6 +514,13 @@ def main() -> int:
             recompute["kl"] = kl_leg(s, model, kv, seqs, P, adv, kept2, ro.logprobs[kept_l], kept_l, N, T)
             log(f"kl: {recompute['kl']}")
 
+    other = None
+    if not args.no_legs and args.workload == "1.5b-b1024" and not args.gen_len:
+        del ro
+        torch.cuda.empty_cache()
+        log("legs: other workloads, one timed rollout each ...")
+        other = legs(model, wl, args.legs_seconds)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
@@ -443,6 +551,7 @@ def main() -> int:
         "kernel_ms_per_rollout": per_step,
         "kept_fraction": kept_frac,
         "recompute": recompute,
+        "legs": other,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -24,9 +24,12 @@
  *     last failure on the calling thread.
  *   - Pointers named d_* are device memory owned by the caller; h_* are host
  *     memory owned by the caller.  The library never allocates device memory:
- *     weights, KV pool, page table and workspaces are caller buffers.  Handles
- *     (dash_model, dash_kv) are library-owned host objects; a dash_kv also owns
- *     a small pinned host staging ring for page-table uploads.
+ *     weights, KV pool, page table and workspaces are caller buffers (the only
+ *     device memory of its own is a 4-byte variable of the diagnostic
+ *     dash_sampler_check, part of the loaded code).  Handles (dash_model,
+ *     dash_kv) are library-owned host objects; a dash_kv also owns a small
+ *     pinned host staging ring for page-table uploads, and kernel timing
+ *     (dash_profile_enable) creates HIP events.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *     compute calls enqueue work on it and return without synchronising;
  *     device outputs are valid after the stream has been synchronised.
@@ -46,7 +49,7 @@
 extern "C" {
 #endif
 
-#define DASH_ABI_VERSION 1
+#define DASH_ABI_VERSION 2
 
 typedef enum dash_status {
     DASH_OK = 0,
@@ -186,8 +189,19 @@ int dash_kv_reserve(dash_kv* kv, const int32_t* h_slots, int32_t n, int32_t new_
  * bookkeeping: pages are reused only by later stream-ordered work. */
 int dash_kv_release(dash_kv* kv, const int32_t* h_slots, int32_t n);
 
-/* Read (and clear) the device status word after synchronising `stream`.
- * Bit 0: a kernel met a position without a backing page (write skipped). */
+/* Device status bits.  Faults found inside kernels are recorded as sticky bits
+ * of a status word instead of stopping the stream:
+ *   DASH_ST_UNBACKED          a position without a backing page was met (its
+ *                             cache write was skipped);
+ *   DASH_ST_NO_FINITE_LOGIT   a sampled row had no finite logit (its token is -1);
+ *   DASH_ST_BAD_TOKEN         a token fed to the decoder was outside [0, vocab)
+ *                             (its hidden-state row, and all that depends on it,
+ *                             is NaN; the id is never used as an index). */
+enum { DASH_ST_UNBACKED = 1u, DASH_ST_NO_FINITE_LOGIT = 2u, DASH_ST_BAD_TOKEN = 4u };
+
+/* Read (and clear) the device status word of a cache after synchronising
+ * `stream`: the bits set by dash_prefill, dash_decode_step, the teacher-forced
+ * calls and dash_rollout (which also records its sampler's bits here). */
 int dash_kv_device_status(dash_kv* kv, uint32_t* out, void* stream);
 
 /* ---- workspace ---------------------------------------------------------- */
@@ -221,10 +235,14 @@ int dash_prefill(dash_model* model, dash_kv* kv, const int32_t* d_prompt_tokens,
                  void* d_ws, size_t ws_bytes, void* stream);
 
 /*
- * One decode step over n_rows rows.  Row b feeds token d_tokens[b] at position
+ * One decode step over n_rows rows: every token of a trajectory is drawn from
+ * pi_theta(. | x, y_<t) (Sec. 3 problem statement, Eq. (1)), and preemptive
+ * sampling runs the whole large batch of samples through the policy at once
+ * (Sec. 3.4); this call computes those next-token distributions, as logits,
+ * for one position of every row.  Row b feeds token d_tokens[b] at position
  * d_pos[b] of slot d_slots[b]: its K/V are appended to the cache at that
  * position and float32 d_logits [n_rows, vocab] receives the next-token
- * logits.  Positions must be backed by pages (dash_kv_reserve with
+ * logits.  A token outside [0, vocab) sets DASH_ST_BAD_TOKEN.  Positions must be backed by pages (dash_kv_reserve with
  * new_len > pos); the kernels skip unbacked writes and set status bit 0.
  * Attention of row b covers positions 0..d_pos[b] of its slot.  Steps over
  * disjoint slots may run at the same time on different streams, each with its
@@ -251,7 +269,10 @@ int dash_decode_step_grouped(dash_model* model, dash_kv* kv, const int32_t* d_to
                              void* stream);
 
 /*
- * Temperature sampling by Gumbel-max with counter-based noise.
+ * Temperature sampling by Gumbel-max with counter-based noise: the draw
+ * y_t ~ pi_theta(. | x, y_<t) of Sec. 3 (problem statement, Eq. (1)) for every
+ * sample of the batch, G samples per prompt (Sec. 3.4), at temperature T (pure
+ * temperature sampling: the paper names no top-k / top-p filter).
  * Row b reads float32 logits row r = d_row_of ? d_row_of[b] : b at
  * d_logits + r * ld, and draws token argmax_v (l_v / T + g_v) over finite l_v
  * (ties to the smallest v; -1 if no l_v is finite), which is a draw from
@@ -262,12 +283,17 @@ int dash_decode_step_grouped(dash_model* model, dash_kv* kv, const int32_t* d_to
  * series 2 atanh((m - 1)/(m + 1)), each operation rounded separately), so a
  * draw depends only on (seed, seq_uid, step, logits) and is bit-reproducible.
  * d_tokens_out [n_rows] int32; d_logprob_out [n_rows] float32 (nullable):
- * log softmax(l / T) at the drawn token.  DASH_EINVAL if temperature <= 0 or
- * not finite, vocab < 1, or ld < vocab.
+ * log softmax(l / T) at the drawn token; d_row_max_lse [n_rows, 2] float32
+ * (nullable): per row m = max_v l_v / T and ln sum_v exp(l_v / T), so that
+ * log softmax(l / T)_v = l_v / T - that second value for any v (both NaN for a
+ * row without a finite logit); d_status (nullable, device uint32): bits OR-ed
+ * in, DASH_ST_NO_FINITE_LOGIT when a row has no finite logit.  DASH_EINVAL if
+ * temperature <= 0 or not finite, vocab < 1, or ld < vocab.
  */
 int dash_sample(const float* d_logits, int64_t ld, int32_t n_rows, int32_t vocab, const int32_t* d_row_of,
                 const int32_t* d_seq_uid, const int32_t* d_step, float temperature, uint64_t seed,
-                int32_t* d_tokens_out, float* d_logprob_out, void* stream);
+                int32_t* d_tokens_out, float* d_logprob_out, float* d_row_max_lse, uint32_t* d_status,
+                void* stream);
 
 /*
  * Self-check of the sampler's screening.  dash_sample first scores every entry
@@ -276,8 +302,9 @@ int dash_sample(const float* d_logits, int64_t ld, int32_t n_rows, int32_t vocab
  * the tolerance of the exact one for every possible u.  This call measures the
  * largest |cheap - exact| over all 2^23 values u can take, on the current
  * device, and returns it with the tolerance the sampler assumes (h_max_err <
- * h_tol means the screening is exact here).  Synchronous; allocates 256 bytes
- * of device memory for the duration of the call.
+ * h_tol means the screening is exact here).  Synchronous (null stream); the
+ * maximum is reduced into a device variable of the library, so the call
+ * allocates nothing.
  */
 int dash_sampler_check(double* h_max_err, double* h_tol);
 

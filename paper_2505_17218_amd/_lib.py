@@ -13,6 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdash.so")
 
 DASH_OK, DASH_EINVAL, DASH_ENOMEM, DASH_ECAPACITY, DASH_EDEVICE, DASH_ENOTSUP = range(6)
+# device status bits (dash_kv_device_status, dash_sample's status word)
+DASH_ST_UNBACKED, DASH_ST_NO_FINITE_LOGIT, DASH_ST_BAD_TOKEN = 1, 2, 4
 DASH_F32, DASH_BF16 = 0, 1
 DASH_ADV_MEAN_ONLY, DASH_ADV_STD_POP, DASH_ADV_STD_SAMPLE, DASH_ADV_LOO = 0, 1, 2, 3
 K_CLASSES = ["prefill", "embed", "norm", "rope", "gemm_qkv", "attn", "attn_combine", "gemm_o", "gemm_gate_up",
@@ -60,7 +62,8 @@ _SIGS = {
     "dash_decode_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P, C.c_size_t, _P]),
     "dash_decode_step_grouped": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, C.c_int32, C.c_int32, C.c_int32, _P,
                                            _P, C.c_size_t, _P]),
-    "dash_sample": (C.c_int, [_P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P, C.c_float, C.c_uint64, _P, _P, _P]),
+    "dash_sample": (C.c_int, [_P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P, C.c_float, C.c_uint64, _P, _P, _P,
+                              _P, _P]),
     "dash_sampler_check": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_double)]),
     "dash_group_advantage_filter": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float, _P, _P,
                                               _P, _P]),
@@ -221,9 +224,9 @@ def dash_decode_step_grouped(model, kv, d_tokens, d_slots, d_pos, n_rows, d_grou
 
 
 def dash_sample(d_logits, ld, n_rows, vocab, d_row_of, d_seq_uid, d_step, temperature, seed, d_tokens_out,
-                d_logprob_out, stream):
+                d_logprob_out, d_row_max_lse, d_status, stream):
     _call("dash_sample", d_logits, ld, n_rows, vocab, d_row_of, d_seq_uid, d_step, C.c_float(temperature),
-          C.c_uint64(seed), d_tokens_out, d_logprob_out, stream)
+          C.c_uint64(seed), d_tokens_out, d_logprob_out, d_row_max_lse, d_status, stream)
 
 
 def dash_group_advantage_filter(d_rewards, n_groups, group, mode, eps, tau, d_adv, d_kept_idx, d_kept_count, stream):

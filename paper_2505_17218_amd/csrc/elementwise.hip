@@ -42,17 +42,28 @@ DASH_DEV float4 load4<bf16_t>(const bf16_t* p) {
 DASH_DEV float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 DASH_DEV float dot4(float4 a) { return a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w; }
 
-// x[r] = E[tok[r]]; y[r] = RMSNorm(x[r]) * w.
+// x[r] = E[tok[r]]; y[r] = RMSNorm(x[r]) * w.  A token outside [0, vocab) is never
+// used as an index: the row becomes NaN (so everything computed from it shows it)
+// and bit 2 of the status word is set.
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads) embed_rmsnorm_k(const int32_t* __restrict__ tok,
                                                                const T* __restrict__ E,
                                                                const T* __restrict__ w, float* __restrict__ x,
-                                                               T* __restrict__ y, int d, int vocab, float eps) {
+                                                               T* __restrict__ y, int d, int vocab, float eps,
+                                                               uint32_t* __restrict__ status) {
     __shared__ float red[kRowThreads / 64];
     const int r = blockIdx.x;
-    int t = tok[r];
-    t = t < 0 ? 0 : (t >= vocab ? vocab - 1 : t);  // never index outside the table
+    const int t = tok[r];
     const int d4 = d >> 2;
+    if (t < 0 || t >= vocab) {  // the same for the whole workgroup
+        const float4 nan4 = make_float4(NAN, NAN, NAN, NAN);
+        for (int i = threadIdx.x; i < d4; i += kRowThreads) {
+            *reinterpret_cast<float4*>(x + (size_t)r * d + 4 * i) = nan4;
+            store4(y + (size_t)r * d + 4 * i, nan4);
+        }
+        if (status && threadIdx.x == 0) atomicOr(status, 4u);
+        return;
+    }
     float4 v[kMaxV];
     float ss = 0.f;
 #pragma unroll
@@ -240,16 +251,16 @@ inline unsigned cdiv(size_t a, size_t b) { return (unsigned)((a + b - 1) / b); }
 }  // namespace
 
 hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, const void* w, float* x, void* y,
-                                int rows, int d, int vocab, float eps, hipStream_t st) {
+                                int rows, int d, int vocab, float eps, uint32_t* status, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     if (d % 4 || d > kRowThreads * 4 * kMaxV) return hipErrorInvalidValue;
     const unsigned blocks = (unsigned)rows;
     if (dtype == 1)
         embed_rmsnorm_k<bf16_t><<<blocks, kRowThreads, 0, st>>>(tok, (const bf16_t*)E, (const bf16_t*)w, x,
-                                                                (bf16_t*)y, d, vocab, eps);
+                                                                (bf16_t*)y, d, vocab, eps, status);
     else
         embed_rmsnorm_k<float><<<blocks, kRowThreads, 0, st>>>(tok, (const float*)E, (const float*)w, x, (float*)y,
-                                                               d, vocab, eps);
+                                                               d, vocab, eps, status);
     return hipGetLastError();
 }
 

@@ -10,10 +10,11 @@
 namespace dash {
 
 // ---- elementwise (elementwise.hip) ----
-// x[r] = E[tok[r]] (fp32); y[r] = RMSNorm(x[r]) * w in the model dtype.
-// Token ids are clamped to [0, vocab) so a bad id can never index outside E.
+// x[r] = E[tok[r]] (fp32); y[r] = RMSNorm(x[r]) * w in the model dtype.  A token id
+// outside [0, vocab) is never used as an index: its rows of x and y become NaN and
+// bit 2 of *status (nullable) is set.
 hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, const void* w, float* x, void* y,
-                                int rows, int d, int vocab, float eps, hipStream_t st);
+                                int rows, int d, int vocab, float eps, uint32_t* status, hipStream_t st);
 // For output row i, r = row_map ? row_map[i] : i: v = x[r] + sum_s delta[s*split_stride + r*d];
 // if write_x, x[r] = v; y[i] = RMSNorm(v) * w.
 hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nsplit, size_t split_stride,
@@ -115,15 +116,19 @@ hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos
                                     int n_heads, void* o, int rows, int prompt_len, hipStream_t st);
 
 // ---- sampling / advantage (sampler.hip, advantage.hip) ----
-// Screening tolerance of the sampler, and an exhaustive check of it: the largest
-// |cheap noise - exact noise| over all noise values, as float bits, max-reduced
-// into *d_max_err_bits (which must start at 0).
+// Screening tolerance of the sampler, and an exhaustive check of it (synchronous, on
+// the null stream): the largest |cheap noise - exact noise| over all noise values.
 float sampler_screen_tol();
-hipError_t launch_sampler_screen_check(unsigned* d_max_err_bits, hipStream_t st);
+hipError_t sampler_screen_check(float* max_err);
+// Row b samples logits row row_of ? row_of[b] : b.  Optional outputs: lp_out [rows]
+// (log-prob of the drawn token), row_ml [rows][2] (max of l/T and the log of the
+// normaliser), traj / traj_lp (the token and log-prob also stored at
+// [uid][step] with row stride traj_ld).  A row without a finite logit draws -1
+// and sets bit 1 of *status (nullable).
 hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
                          const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
-                         int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,
-                         hipStream_t st);
+                         int32_t* tok_out, float* lp_out, float* row_ml, uint32_t* status, int32_t* traj,
+                         float* traj_lp, int traj_ld, hipStream_t st);
 // lp_out[b] = log softmax(logits row b)[y_b] with y_b = tokens[(b / per) * stride + off + b % per]
 // (rows grouped per sequence: `per` scored positions of a sequence whose tokens
 // start every `stride` entries, the first scored token at `off`); NaN for a token

@@ -711,7 +711,7 @@ int decode_step_impl(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
     {
         ProfScope ps(DASH_K_EMBED, st);
         DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab,
-                                      d.rms_eps, st));
+                                      d.rms_eps, kv->d_status, st));
     }
     int sd = 1;
     int rc = run_layers(m, kv, w, rows, pos, slot, false, 0, st, &sd, gi);
@@ -766,7 +766,7 @@ int prefill_impl(dash_model* m, dash_kv* kv, const int32_t* d_tokens, int n_prom
         if ((rc = kv_upload(kv, w.slot, slot.data(), rows * 4, st))) return rc;
         if ((rc = kv_upload(kv, w.gather, gather.data(), np * 4, st))) return rc;
         DASH_HIP(launch_embed_rmsnorm(d.dtype, d_tokens + (size_t)p0 * P, m->embed(), m->lw(0, 0), w.x, w.y, rows,
-                                      d.d_model, d.vocab, d.rms_eps, st));
+                                      d.d_model, d.vocab, d.rms_eps, kv->d_status, st));
         int sd = 1;
         if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, P, st, &sd, nullptr))) return rc;
         // final norm of the last position of every prompt only
@@ -841,29 +841,22 @@ int dash_decode_step_grouped(dash_model* m, dash_kv* kv, const int32_t* tok, con
 
 int dash_sample(const float* logits, int64_t ld, int32_t rows, int32_t vocab, const int32_t* row_of,
                 const int32_t* uid, const int32_t* step, float temperature, uint64_t seed, int32_t* tok_out,
-                float* lp_out, void* stream) {
+                float* lp_out, float* row_max_lse, uint32_t* d_status, void* stream) {
     if (!logits || !uid || !step || !tok_out) return fail(DASH_EINVAL, "dash_sample: NULL argument");
     if (rows < 0 || vocab < 1 || ld < vocab) return fail(DASH_EINVAL, "dash_sample: bad sizes");
     if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DASH_EINVAL, "temperature must be > 0 and finite");
     if (rows == 0) return DASH_OK;
     ProfScope ps(DASH_K_SAMPLE, (hipStream_t)stream);
-    DASH_HIP(launch_sample(logits, ld, rows, vocab, row_of, uid, step, temperature, seed, tok_out, lp_out, nullptr,
-                           nullptr, 0, (hipStream_t)stream));
+    DASH_HIP(launch_sample(logits, ld, rows, vocab, row_of, uid, step, temperature, seed, tok_out, lp_out, row_max_lse,
+                           d_status, nullptr, nullptr, 0, (hipStream_t)stream));
     return DASH_OK;
 }
 
 int dash_sampler_check(double* h_max_err, double* h_tol) {
     if (!h_max_err || !h_tol) return fail(DASH_EINVAL, "dash_sampler_check: NULL argument");
-    unsigned* d = nullptr;
-    DASH_HIP(hipMalloc(&d, 256));
-    unsigned bits = 0;
-    hipError_t e = hipMemset(d, 0, 4);
-    if (e == hipSuccess) e = launch_sampler_screen_check(d, nullptr);
-    if (e == hipSuccess) e = hipMemcpy(&bits, d, 4, hipMemcpyDeviceToHost);
-    (void)hipFree(d);
+    float f = 0.f;
+    const hipError_t e = sampler_screen_check(&f);
     if (e != hipSuccess) return fail(DASH_EDEVICE, "sampler check: %s", hipGetErrorString(e));
-    float f;
-    memcpy(&f, &bits, 4);
     *h_max_err = f;
     *h_tol = sampler_screen_tol();
     return DASH_OK;
@@ -960,7 +953,7 @@ int tf_forward(dash_model* m, dash_kv* kv, const Ws& w, const int32_t* tok, int 
                float* logits, hipStream_t st) {
     const auto& d = m->d;
     DASH_HIP(launch_embed_rmsnorm(d.dtype, tok, m->embed(), m->lw(0, 0), w.x, w.y, rows, d.d_model, d.vocab, d.rms_eps,
-                                  st));
+                                  kv->d_status, st));
     int sd = 1, rc;
     if ((rc = run_layers(m, kv, w, rows, w.pos, w.slot, true, L, st, &sd, nullptr))) return rc;
     // final norm of the positions that predict a completion token, then the LM head
@@ -1238,8 +1231,8 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
     int32_t** S = rw.st[cur];  // tok, slot, pos, step, uid
     DASH_HIP(launch_rows_init(S[1], S[4], S[2], S[3], N, P - 1, 0, st));
     DASH_HIP(launch_iota_div(rw.row_of, N, G, st));
-    DASH_HIP(launch_sample(rw.logits, V, N, V, rw.row_of, S[4], S[3], temperature, seed, S[0], nullptr, d_out_tokens,
-                           d_out_lp, T, st));
+    DASH_HIP(launch_sample(rw.logits, V, N, V, rw.row_of, S[4], S[3], temperature, seed, S[0], nullptr, nullptr,
+                           kv->d_status, d_out_tokens, d_out_lp, T, st));
     // live rows after each step are known on the host from the budgets
     std::vector<int> live_after(T + 1, 0);  // rows live for step t (t >= 1): budget > t
     for (int i = 0; i < N; ++i)
@@ -1284,8 +1277,8 @@ int dash_rollout(dash_model* m, dash_kv* kv, const int32_t* d_prompts, int32_t n
         if (rc2) return rc2;
         {
             ProfScope ps(DASH_K_SAMPLE, st);
-            DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr,
-                                   d_out_tokens, d_out_lp, T, st));
+            DASH_HIP(launch_sample(rw.logits, V, B, V, nullptr, S[4], S[3], temperature, seed, S[0], nullptr, nullptr,
+                                   kv->d_status, d_out_tokens, d_out_lp, T, st));
         }
         ProfScope ps(DASH_K_OTHER, st);
         return advance(B);

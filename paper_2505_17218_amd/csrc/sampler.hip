@@ -21,6 +21,8 @@
 // every entry exactly.  Before the cheap noise, an upper bound on the exact noise
 // read off the random word's leading ones (noise_bound) already rules out almost
 // every entry once the bound has risen, without any logarithm.
+#include <cstring>
+
 #include "common.h"
 #include "kernels.h"
 #include "sampler_math.h"
@@ -86,8 +88,9 @@ template <bool UNIT_T>
 __global__ void __launch_bounds__(kThreads)
 sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ row_of,
          const int32_t* __restrict__ uid, const int32_t* __restrict__ step, float temperature, uint32_t k0,
-         uint32_t k1, int32_t* __restrict__ tok_out, float* __restrict__ lp_out, int32_t* __restrict__ traj,
-         float* __restrict__ traj_lp, int traj_ld, int vec4) {
+         uint32_t k1, int32_t* __restrict__ tok_out, float* __restrict__ lp_out, float* __restrict__ row_ml,
+         uint32_t* __restrict__ status, int32_t* __restrict__ traj, float* __restrict__ traj_lp, int traj_ld,
+         int vec4) {
     __shared__ float red_s[kThreads / 64];
     __shared__ int red_i[kThreads / 64];
     __shared__ float red_m[kThreads / 64];
@@ -184,20 +187,32 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
         mx = nm;
     }
     int tok = -1;
-    float lp = NAN;
+    float lp = NAN, lse = NAN;
     if (best_i != 0x7FFFFFFF) {
         tok = best_i;
         const float sc = UNIT_T ? row[tok] : div_rn(row[tok], temperature);
-        lp = sc - mx - logf(z);
+        const float lz = logf(z);
+        lp = sc - mx - lz;
+        lse = mx + lz;
+    } else if (status) {
+        atomicOr(status, 2u);  // no finite logit: nothing can be drawn
     }
     tok_out[b] = tok;
     if (lp_out) lp_out[b] = lp;
+    if (row_ml) {
+        row_ml[2 * (size_t)b] = tok >= 0 ? mx : NAN;
+        row_ml[2 * (size_t)b + 1] = lse;
+    }
     if (traj) traj[(size_t)u_id * traj_ld + st] = tok;
     if (traj_lp) traj_lp[(size_t)u_id * traj_ld + st] = lp;
 }
 
 // Largest |cheap noise - exact noise| over every value u can take: (x >> 8) | 1
-// is odd, so x = (2k + 1) << 8 for k < 2^23 covers them all.
+// is odd, so x = (2k + 1) << 8 for k < 2^23 covers them all.  The maximum (float
+// bits, max-reduced) lands in a device variable of this file, so the check needs
+// no allocation.
+__device__ unsigned g_screen_max_err;
+
 __global__ void screen_check_k(unsigned* max_err_bits) {
     const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= (1u << 23)) return;
@@ -379,23 +394,34 @@ hipError_t launch_logits_kl(const float* theta, const float* base, int64_t ld, i
 
 float sampler_screen_tol() { return kScreenTol; }
 
-hipError_t launch_sampler_screen_check(unsigned* d_max_err_bits, hipStream_t st) {
-    screen_check_k<<<(1 << 23) / 256, 256, 0, st>>>(d_max_err_bits);
-    return hipGetLastError();
+hipError_t sampler_screen_check(float* max_err) {
+    unsigned* d = nullptr;
+    hipError_t e = hipGetSymbolAddress((void**)&d, HIP_SYMBOL(g_screen_max_err));
+    if (e != hipSuccess) return e;
+    const unsigned zero = 0;
+    if ((e = hipMemcpy(d, &zero, 4, hipMemcpyHostToDevice)) != hipSuccess) return e;
+    screen_check_k<<<(1 << 23) / 256, 256, 0, nullptr>>>(d);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    unsigned bits = 0;
+    if ((e = hipMemcpy(&bits, d, 4, hipMemcpyDeviceToHost)) != hipSuccess) return e;
+    std::memcpy(max_err, &bits, 4);
+    return hipSuccess;
 }
 
 hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, const int32_t* row_of,
                          const int32_t* uid, const int32_t* step, float temperature, uint64_t seed,
-                         int32_t* tok_out, float* lp_out, int32_t* traj, float* traj_lp, int traj_ld,
-                         hipStream_t st) {
+                         int32_t* tok_out, float* lp_out, float* row_ml, uint32_t* status, int32_t* traj,
+                         float* traj_lp, int traj_ld, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
     if (temperature == 1.0f)
         sample_k<true><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
-                                                  (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
+                                                  (uint32_t)(seed >> 32), tok_out, lp_out, row_ml, status, traj,
+                                                  traj_lp, traj_ld, vec4);
     else
         sample_k<false><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, (uint32_t)seed,
-                                                   (uint32_t)(seed >> 32), tok_out, lp_out, traj, traj_lp, traj_ld, vec4);
+                                                   (uint32_t)(seed >> 32), tok_out, lp_out, row_ml, status, traj,
+                                                   traj_lp, traj_ld, vec4);
     return hipGetLastError();
 }
 

@@ -147,14 +147,16 @@ def decode_step_grouped(model: Model, kv: KVCache, tokens: torch.Tensor, slots: 
 
 
 def sample(logits: torch.Tensor, seq_uid: torch.Tensor, step: torch.Tensor, temperature: float, seed: int,
-           row_of: torch.Tensor | None = None, n_rows: int | None = None, with_logprob: bool = True):
-    """dash_sample: returns (int32 tokens [n_rows], float32 logprobs [n_rows] or None)."""
+           row_of: torch.Tensor | None = None, n_rows: int | None = None, with_logprob: bool = True,
+           row_max_lse: torch.Tensor | None = None, status: torch.Tensor | None = None):
+    """dash_sample: returns (int32 tokens [n_rows], float32 logprobs [n_rows] or None).
+    Optional outputs: row_max_lse float32 [n_rows, 2]; status uint32/int32 [1] (bits OR-ed in)."""
     n = seq_uid.numel() if n_rows is None else n_rows
     V = logits.shape[-1]
     toks = torch.empty(n, dtype=torch.int32, device=logits.device)
     lps = torch.empty(n, dtype=torch.float32, device=logits.device) if with_logprob else None
     L.dash_sample(logits.data_ptr(), logits.stride(0), n, V, L.ptr(row_of), seq_uid.data_ptr(), step.data_ptr(),
-                  temperature, seed, toks.data_ptr(), L.ptr(lps), stream_handle())
+                  temperature, seed, toks.data_ptr(), L.ptr(lps), L.ptr(row_max_lse), L.ptr(status), stream_handle())
     return toks, lps
 
 

@@ -35,8 +35,10 @@ class StepRun:
 
 
 def run_stepwise(model: engine.Model, kv: engine.KVCache, prompts: np.ndarray, group: int, gen_len: int,
-                 temperature: float, seed: int, keep_logits: bool = True) -> StepRun:
-    """Prefill, then gen_len - 1 decode steps, sampling after each; all through the C ABI."""
+                 temperature: float, seed: int, keep_logits: bool = True, grouped: bool = False) -> StepRun:
+    """Prefill, then gen_len - 1 decode steps, sampling after each; all through the C ABI.
+    grouped: decode with dash_decode_step_grouped (each prompt's samples as one
+    prefix-sharing group over the prompt's full pages)."""
     n_prompts, P = prompts.shape
     N = n_prompts * group
     V = model.shape.vocab
@@ -55,10 +57,16 @@ def run_stepwise(model: engine.Model, kv: engine.KVCache, prompts: np.ndarray, g
     if keep_logits:
         all_logits[0] = logits0.cpu().numpy()[np.arange(N) // group]
     ws = model.workspace(N, kv.max_ctx)
+    group_off = dev_i32(np.arange(0, N + 1, group))
+    shared = P // kv.page_size * kv.page_size
     for t in range(1, gen_len):
         pos = P + t - 1
         engine.L.dash_kv_reserve(kv.handle, slots, pos + 1, engine.stream_handle())
-        logits = engine.decode_step(model, kv, tok, slot_t, dev_i32(np.full(N, pos)), ws=ws)
+        if grouped:
+            logits = engine.decode_step_grouped(model, kv, tok, slot_t, dev_i32(np.full(N, pos)), group_off, group,
+                                                shared, ws=ws)
+        else:
+            logits = engine.decode_step(model, kv, tok, slot_t, dev_i32(np.full(N, pos)), ws=ws)
         tok, lp = engine.sample(logits, uid, dev_i32(np.full(N, t)), temperature, seed)
         toks[:, t] = tok.cpu().numpy()
         lps[:, t] = lp.cpu().numpy()

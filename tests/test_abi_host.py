@@ -36,7 +36,7 @@ def test_header_symbols_exported():
 
 
 def test_version_and_status_strings():
-    assert L.dash_abi_version() == 1
+    assert L.dash_abi_version() == 2
     lib = L.load()
     for s in range(6):
         assert lib.dash_status_str(s)
@@ -87,16 +87,16 @@ def test_model_create_validation():
 
 def test_sample_and_advantage_validation():
     with pytest.raises(L.DashError) as e:
-        L.dash_sample(0x1000, 512, 4, 512, None, 0x2000, 0x3000, 0.0, 1, 0x4000, None, None)
+        L.dash_sample(0x1000, 512, 4, 512, None, 0x2000, 0x3000, 0.0, 1, 0x4000, None, None, None, None)
     assert e.value.status == L.DASH_EINVAL
     with pytest.raises(L.DashError) as e:
-        L.dash_sample(0x1000, 100, 4, 512, None, 0x2000, 0x3000, 1.0, 1, 0x4000, None, None)
+        L.dash_sample(0x1000, 100, 4, 512, None, 0x2000, 0x3000, 1.0, 1, 0x4000, None, None, None, None)
     assert e.value.status == L.DASH_EINVAL
     with pytest.raises(L.DashError) as e:
-        L.dash_sample(0x1000, 512, 4, 512, None, 0x2000, 0x3000, float("nan"), 1, 0x4000, None, None)
+        L.dash_sample(0x1000, 512, 4, 512, None, 0x2000, 0x3000, float("nan"), 1, 0x4000, None, None, None, None)
     assert e.value.status == L.DASH_EINVAL
     # zero rows is a no-op, not an error
-    L.dash_sample(0x1000, 512, 0, 512, None, 0x2000, 0x3000, 1.0, 1, 0x4000, None, None)
+    L.dash_sample(0x1000, 512, 0, 512, None, 0x2000, 0x3000, 1.0, 1, 0x4000, None, None, None, None)
     for args, want in [((0, 4), L.DASH_EINVAL), ((4, 0), L.DASH_EINVAL), ((1, 65537), L.DASH_ENOTSUP),
                        ((1 << 20, 64), L.DASH_ENOTSUP)]:
         with pytest.raises(L.DashError) as e:

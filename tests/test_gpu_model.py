@@ -471,3 +471,36 @@ def test_unbacked_position_sets_status_and_does_not_fault():
     assert torch.isfinite(logits[0]).all()
     assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) & 1
     assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) == 0
+
+
+def test_bad_token_sets_status_and_poisons_only_its_row():
+    """A token outside [0, vocab) is never used as an index: its row's logits are NaN, the
+    cache's status word gets DASH_ST_BAD_TOKEN, and the other rows' logits are bit-identical
+    to a step in which every token was valid."""
+    shape = BF16_A
+    model = engine.Model(shape, synth.make_weights(shape, 0))
+    kv = make_kv(model, 32, 3, 64)
+    L.dash_kv_reserve(kv.handle, [0, 1, 2], 10, engine.stream_handle())
+    slots, pos = dev_i32([0, 1, 2]), dev_i32([5, 5, 5])
+    good = engine.decode_step(model, kv, dev_i32([1, 2, 3]), slots, pos).cpu().numpy()
+    assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) == 0
+    bad = engine.decode_step(model, kv, dev_i32([1, -1, shape.vocab]), slots, pos).cpu().numpy()
+    assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) == L.DASH_ST_BAD_TOKEN
+    np.testing.assert_array_equal(bad[0], good[0])
+    assert np.isnan(bad[1:]).all()
+    assert L.dash_kv_device_status(kv.handle, engine.stream_handle()) == 0
+
+
+@pytest.mark.parametrize("shape,n_prompts,G,P,T", [(BF16_B, 2, 4, 100, 8), (BF16_A, 2, 8, 600, 4)])
+def test_grouped_decode_matches_oracle(shape, n_prompts, G, P, T):
+    """The prefix-shared decode kernel (each prompt's samples as one group over the prompt's
+    full pages) against the oracle: logits within the bf16 tolerance at every generated
+    position, and the oracle sampler reproduces the tokens from those logits."""
+    w = synth.make_weights(shape, 15)
+    wl = synth.Workload("t", shape, n_prompts, G, P, T)
+    prompts = synth.make_prompts(wl, 15)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, n_prompts * G, P + T)
+    run = run_stepwise(model, kv, prompts, G, T, 1.0, 19, grouped=True)
+    worst = _check_run(shape, w, prompts, G, T, run, 1.0, 19, TOL[shape.dtype])
+    print(f"grouped {shape.name} P={P}: max |dlogits| = {worst:.3g}")

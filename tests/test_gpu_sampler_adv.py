@@ -5,6 +5,7 @@ import pytest
 import torch
 
 from oracle import advantage as oa
+from oracle import rollout as oro
 from oracle import sampler as osm
 from paper_2505_17218_amd import _lib as L
 from paper_2505_17218_amd import engine, synth
@@ -107,9 +108,13 @@ def test_sample_deterministic_and_independent_of_batch_position():
 def test_advantage_filter_bitexact(G, mode):
     """Every mode and group size, from wave-sized groups to one group of 65536 (the
     single-path baseline of Eq. (3) over a whole batch), bit-exact against the oracle."""
-    if mode == L.DASH_ADV_LOO and G == 1:
-        pytest.skip("the leave-one-out baseline needs two samples")
     n_groups = max(1, 4096 // G)
+    if mode == L.DASH_ADV_LOO and G == 1:  # the leave-one-out baseline needs two samples per group
+        r = torch.zeros(n_groups, dtype=torch.float32, device="cuda")
+        with pytest.raises(L.DashError) as e:
+            engine.advantage_filter(r, 1, mode, 1e-6, 0.1)
+        assert e.value.status == L.DASH_EINVAL
+        return
     r = synth.make_rewards(n_groups, G, "beta0.5", seed=G)
     # mix in continuous rewards so |A| lands everywhere, including near tau
     cont = np.random.default_rng(G).standard_normal(r.size).astype(np.float32) * np.float32(0.3)
@@ -140,23 +145,65 @@ def test_advantage_tau_zero_and_tiny():
     np.testing.assert_array_equal(kept1.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("n,eos", [(1, -1), (1000, -1), (4096, 7), (3000, -1)])
-def test_live_compact(n, eos):
-    rng = np.random.default_rng(n)
-    uid = rng.permutation(8192)[:n].astype(np.int32)
-    budget = rng.integers(1, 50, 8192).astype(np.int32)
+@pytest.mark.parametrize("n,eos", [(0, -1), (1, -1), (1000, -1), (4096, 7), (3000, -1), (9000, 3)])
+def test_live_compact_matches_oracle(n, eos):
+    """dash_live_compact against the oracle's row bookkeeping (oracle.rollout.live_compact),
+    bit for bit: which rows go on, their order, and their advanced positions and steps."""
+    rng = np.random.default_rng(n + 1)
+    uid = rng.permutation(16384)[:n].astype(np.int32)
+    budget = rng.integers(1, 50, 16384).astype(np.int32)
     step = rng.integers(0, 50, n).astype(np.int32)
     tok = rng.integers(0, 16, n).astype(np.int32)
     slot = rng.integers(0, 1 << 16, n).astype(np.int32)
     pos = rng.integers(0, 4096, n).astype(np.int32)
-    outs = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in range(5)]
-    cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
-    ins = [dev_i32(a) for a in (tok, slot, pos, step, uid)]
+    m = max(n, 1)
+    outs = [torch.full((m,), -7, dtype=torch.int32, device="cuda") for _ in range(5)]
+    cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    ins = [dev_i32(a if n else np.zeros(1)) for a in (tok, slot, pos, step, uid)]
     L.dash_live_compact(*[t.data_ptr() for t in ins], dev_i32(budget).data_ptr(), eos, n,
                         *[t.data_ptr() for t in outs], cnt.data_ptr(), engine.stream_handle())
-    live = (step + 1 < budget[uid]) & ~((eos >= 0) & (tok == eos))
+    want = oro.live_compact(tok, slot, pos, step, uid, budget, eos)
     k = int(cnt.item())
-    assert k == live.sum()
-    got = [t.cpu().numpy()[:k] for t in outs]
-    for g, w in zip(got, (tok[live], slot[live], pos[live] + 1, step[live] + 1, uid[live])):
-        np.testing.assert_array_equal(g, w)
+    assert k == len(want[0])
+    for g, w in zip(outs, want):
+        np.testing.assert_array_equal(g.cpu().numpy()[:k], w)
+        assert (g.cpu().numpy()[k:] == -7).all()  # nothing written past the live rows
+
+
+def test_sample_status_bit_and_row_max_lse():
+    """A row with no finite logit draws -1 and sets DASH_ST_NO_FINITE_LOGIT in the status word;
+    non-finite entries are never drawn; the per-row (max, log normaliser) output matches the
+    float64 values of softmax(l / T), and the drawn token's log-prob equals l / T minus it."""
+    rows, V, temp, seed = 6, 1000, 0.8, 9
+    lg = synth.make_logits(rows, V, seed=5, scale=2.0)
+    lg[1, :] = np.nan                 # nothing finite
+    lg[2, :] = -np.inf
+    lg[2, 17] = 0.5                   # one finite entry
+    lg[3, 5] = np.inf                 # never drawn
+    lg[4, :] = -np.inf                # nothing finite
+    d = torch.from_numpy(lg).cuda()
+    ml = torch.full((rows, 2), 7.0, dtype=torch.float32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    uid, step = dev_i32(np.arange(rows)), dev_i32(np.zeros(rows))
+    toks, lps = engine.sample(d, uid, step, temp, seed, row_max_lse=ml, status=st)
+    want, want_lp = osm.sample(lg, np.arange(rows), np.zeros(rows), temp, seed)
+    toks = toks.cpu().numpy()
+    np.testing.assert_array_equal(toks, want)
+    assert want[1] == -1 and want[4] == -1 and want[2] == 17 and want[3] != 5
+    assert int(st.item()) == L.DASH_ST_NO_FINITE_LOGIT
+    ml, lps = ml.cpu().numpy(), lps.cpu().numpy()
+    T32 = np.float32(temp)
+    for r in (0, 2, 3, 5):
+        z = (lg[r][np.isfinite(lg[r])] / T32).astype(np.float64)
+        m = z.max()
+        lse = m + np.log(np.exp(z - m).sum())
+        assert ml[r, 0] == np.float32(m)
+        assert abs(ml[r, 1] - lse) <= LP_ATOL + LP_RTOL * abs(lse)
+        assert abs(lps[r] - (np.float32(lg[r, toks[r]] / T32) - ml[r, 1])) <= 1e-5
+    assert np.isnan(ml[[1, 4]]).all() and np.isnan(lps[[1, 4]]).all()
+    # rows with finite logits only: the bit stays clear; no status pointer is fine too
+    st.zero_()
+    engine.sample(d[[0, 2, 3, 5]].contiguous(), dev_i32(np.arange(4)), dev_i32(np.zeros(4)), temp, seed, status=st)
+    engine.sample(d, uid, step, temp, seed)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
