@@ -80,7 +80,7 @@ def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndar
     mask = np.triu(np.ones((S, S), dtype=bool), 1)
     for h in range(Hq):
         kh, vh = k[:, h // rep, :], v[:, h // rep, :]
-        s = (q[:, h, :] @ kh.T) / np.sqrt(hd)
+        s = (q[:, h, :] @ kh.T) / q.dtype.type(np.sqrt(hd))
         s[mask] = -np.inf
         s = s - s.max(axis=1, keepdims=True)
         p = np.exp(s)
@@ -94,7 +94,7 @@ def silu(z: np.ndarray) -> np.ndarray:
 
 
 def forward(shape: dict, weights: dict, tokens: np.ndarray,
-            positions: np.ndarray | None = None) -> np.ndarray:
+            positions: np.ndarray | None = None, arith=np.float64) -> np.ndarray:
     """Next-token logits (float64) of one sequence.
 
     ``shape`` has keys n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff,
@@ -104,20 +104,28 @@ def forward(shape: dict, weights: dict, tokens: np.ndarray,
     l{i}.w_gate_up [2 d_ff, d] (gate rows, then up rows), l{i}.w_down [d, d_ff].
     ``tokens`` int [S] occupy positions 0..S-1.  Returns logits [len(positions), V]
     at the requested positions (default: all).
+
+    ``arith`` (float64 by default) is the floating-point type every operation is
+    evaluated in.  float32 evaluates the same definition with float32 rounding; the
+    tests use it only to measure how far fp32 arithmetic alone moves the logits of a
+    deep bf16 network (through the bf16 storage points) from the float64 values.
     """
     bf = shape["dtype"] == 1
-    rb = round_bf16 if bf else (lambda a: a)
+    A = arith
+    rb = (lambda a: round_bf16(a).astype(A)) if bf else (lambda a: a)
     L, Hq, Hkv, hd = shape["n_layers"], shape["n_heads"], shape["n_kv_heads"], shape["head_dim"]
-    ff, eps = shape["d_ff"], shape["rms_eps"]
+    ff, eps = shape["d_ff"], A(shape["rms_eps"])
+    W = lambda name: as_f64(weights[name]).astype(A, copy=False)
     tokens = np.asarray(tokens)
     S = tokens.shape[0]
-    E = as_f64(weights["embed"])
+    E = W("embed")
     x = E[tokens].copy()
     cos, sin = rope_angles(np.arange(S), hd, shape["rope_theta"])
+    cos, sin = cos.astype(A), sin.astype(A)
     for l in range(L):
         p = f"l{l}."
-        y = rb(rmsnorm(x, as_f64(weights[p + "attn_norm"]), eps))
-        qkv = y @ as_f64(weights[p + "w_qkv"]).T + as_f64(weights[p + "b_qkv"])
+        y = rb(rmsnorm(x, W(p + "attn_norm"), eps))
+        qkv = y @ W(p + "w_qkv").T + W(p + "b_qkv")
         q = qkv[:, :Hq * hd].reshape(S, Hq, hd)
         k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(S, Hkv, hd)
         v = qkv[:, (Hq + Hkv) * hd:].reshape(S, Hkv, hd)
@@ -125,15 +133,15 @@ def forward(shape: dict, weights: dict, tokens: np.ndarray,
         k = rb(rope(k, cos, sin))
         v = rb(v)
         o = rb(causal_gqa_attention(q, k, v).reshape(S, Hq * hd))
-        x = x + o @ as_f64(weights[p + "w_o"]).T
-        y = rb(rmsnorm(x, as_f64(weights[p + "mlp_norm"]), eps))
-        gu = y @ as_f64(weights[p + "w_gate_up"]).T
+        x = x + o @ W(p + "w_o").T
+        y = rb(rmsnorm(x, W(p + "mlp_norm"), eps))
+        gu = y @ W(p + "w_gate_up").T
         h = rb(silu(gu[:, :ff]) * gu[:, ff:])
-        x = x + h @ as_f64(weights[p + "w_down"]).T
+        x = x + h @ W(p + "w_down").T
     if positions is not None:
         x = x[np.asarray(positions)]
-    y = rb(rmsnorm(x, as_f64(weights["final_norm"]), eps))
-    return y @ E.T
+    y = rb(rmsnorm(x, W("final_norm"), eps))
+    return (y @ E.T).astype(np.float64)
 
 
 def rollout_logits(shape: dict, weights: dict, prompt: np.ndarray, generated: np.ndarray) -> np.ndarray:

@@ -298,3 +298,17 @@ def test_rollout_logits_positions(micro):
     lg = om.rollout_logits(shape, w, prompt, gen)
     full = om.forward(shape, w, np.concatenate([prompt, gen]))
     np.testing.assert_allclose(lg, full[3:6], rtol=1e-13)
+
+
+def test_float32_arithmetic_mode(micro):
+    """The float32 evaluation mode computes the same definition: on the float32 micro shape
+    it agrees with the float64 evaluation to float32 precision, keeps float32 intermediates
+    (so it is not float64 in disguise), and leaves the float64 default untouched."""
+    shape, w = micro
+    toks = np.array([3, 1, 4, 1, 5, 9, 2], dtype=np.int32)
+    a64 = om.forward(shape, w, toks)
+    a32 = om.forward(shape, w, toks, arith=np.float32)
+    assert a32.dtype == np.float64
+    np.testing.assert_allclose(a32, a64, rtol=2e-5, atol=2e-5)
+    assert np.abs(a32 - a64).max() > 1e-9
+    np.testing.assert_array_equal(om.forward(shape, w, toks, arith=np.float64), a64)
