@@ -254,6 +254,23 @@ int dash_decode_step(dash_model* model, dash_kv* kv, const int32_t* d_tokens, co
                      void* stream);
 
 /*
+ * dash_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The step's workspace is a 64 MiB device
+ * array inside the library (one per device, created with the loaded code and
+ * held until the process ends); nothing is allocated by the call.  The caller
+ * passes inputs and outputs as for dash_decode_step and gets the same logits
+ * bit for bit.  DASH_ECAPACITY (before any launch) when
+ * dash_workspace_bytes(model, n_rows, kv max_ctx) exceeds 64 MiB (up to 496
+ * rows for the Qwen2.5-1.5B shape at max_ctx 1280, 752 for 0.5B, 361 for 3B at
+ * max_ctx 1536).  Every call on a device shares that
+ * device's array: calls that overlap in time on one device (different streams
+ * or threads) race and give undefined results; serialise them.
+ */
+int dash_decode_step_noalloc(dash_model* model, dash_kv* kv, const int32_t* d_tokens, const int32_t* d_slots,
+                             const int32_t* d_pos, int32_t n_rows, float* d_logits, void* stream);
+
+/*
  * dash_decode_step for a batch made of prefix-sharing groups (the G samples of a
  * prompt after the group fork): rows d_group_off[i] .. d_group_off[i+1]-1 (int32
  * device array of n_groups + 1 ascending offsets, the last equal to n_rows, each

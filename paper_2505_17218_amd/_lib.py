@@ -60,6 +60,7 @@ _SIGS = {
     "dash_workspace_bytes": (C.c_size_t, [_P, C.c_int32, C.c_int32]),
     "dash_prefill": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, _I32P, _P, _P, C.c_size_t, _P]),
     "dash_decode_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P, C.c_size_t, _P]),
+    "dash_decode_step_noalloc": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P]),
     "dash_decode_step_grouped": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, C.c_int32, C.c_int32, C.c_int32, _P,
                                            _P, C.c_size_t, _P]),
     "dash_sample": (C.c_int, [_P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P, C.c_float, C.c_uint64, _P, _P, _P,
@@ -215,6 +216,10 @@ def dash_prefill(model, kv, d_tokens, n_prompts, prompt_len, group, slots, d_log
 
 def dash_decode_step(model, kv, d_tokens, d_slots, d_pos, n_rows, d_logits, d_ws, ws_bytes, stream):
     _call("dash_decode_step", model, kv, d_tokens, d_slots, d_pos, n_rows, d_logits, d_ws, ws_bytes, stream)
+
+
+def dash_decode_step_noalloc(model, kv, d_tokens, d_slots, d_pos, n_rows, d_logits, stream):
+    _call("dash_decode_step_noalloc", model, kv, d_tokens, d_slots, d_pos, n_rows, d_logits, stream)
 
 
 def dash_decode_step_grouped(model, kv, d_tokens, d_slots, d_pos, n_rows, d_group_off, n_groups, group_size,

@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <tuple>
 #include <string>
 #include <vector>
@@ -818,6 +819,63 @@ int dash_decode_step(dash_model* m, dash_kv* kv, const int32_t* tok, const int32
     if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
     if (rows < 1) return fail(DASH_EINVAL, "n_rows must be >= 1");
     int rc = check_ws(m, ws, ws_bytes, rows, kv->max_ctx);
+    if (rc) return rc;
+    return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+// ------------------------------------------- allocation-free decode step ----
+// dash_decode_step_noalloc runs the decode step with its workspace in `scratch`,
+// a device array of this file (one copy per device, held until the process ends).
+// In host code `scratch` names a host-side stand-in, never a device address: the
+// device address comes from hipGetSymbolAddress, once per device, and only that
+// address is handed to kernels.  No kernel of the decode step needs any of the
+// scratch to start at zero (every buffer is written before it is read in the same
+// call), so nothing is cleared between calls.
+
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch (looked up on the first call per device).
+int scratch_address(void** out) {
+    int dev = -1;
+    DASH_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(DASH_ENOTSUP, "device %d beyond the %d supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return fail(DASH_EDEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return DASH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dash_decode_step_noalloc(dash_model* m, dash_kv* kv, const int32_t* tok, const int32_t* slot, const int32_t* pos,
+                             int32_t rows, float* logits, void* stream) {
+    if (!m || !kv || !tok || !slot || !pos || !logits) return fail(DASH_EINVAL, "dash_decode_step_noalloc: NULL argument");
+    if (kv->m != m) return fail(DASH_EINVAL, "kv handle belongs to another model");
+    if (rows < 1) return fail(DASH_EINVAL, "n_rows must be >= 1");
+    if (rows > max_forward_rows(m))
+        return fail(DASH_ENOTSUP, "%d rows exceed the %d one forward pass may hold", rows, max_forward_rows(m));
+    const size_t need = plan_ws(m, rows, nullptr, kv->max_ctx).bytes;
+    if (need > kScratchBytes)
+        return fail(DASH_ECAPACITY, "%d rows need %zu bytes of workspace; the allocation-free decode step has %zu",
+                    rows, need, kScratchBytes);
+    void* ws = nullptr;
+    const int rc = scratch_address(&ws);
     if (rc) return rc;
     return decode_step_impl(m, kv, tok, slot, pos, rows, logits, ws, (hipStream_t)stream);
 }
