@@ -2,8 +2,9 @@
 
 Usage: python -m paper_2505_17218_amd.build   (or __graft_entry__.build()).
 Compiles every library source in csrc/ with hipcc into one shared library next to
-this file, and the native benchmark (csrc/native_bench.hip, a C-ABI client that
-needs no Python) into dash_native_bench beside it.  The sampler and advantage
+this file, the native benchmark (csrc/native_bench.hip, a C-ABI client that needs
+no Python) into dash_native_bench, and the projection-GEMM micro-benchmark
+(csrc/gemm_bench.hip) into dash_gemm_bench beside it.  The sampler and advantage
 kernels are built with -ffp-contract=off: their float32 arithmetic is part of a
 bit-exact contract.
 """
@@ -20,6 +21,7 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libdash.so")
 NATIVE_BENCH = os.path.join(HERE, "dash_native_bench")
+GEMM_BENCH = os.path.join(HERE, "dash_gemm_bench")
 BUILD = os.path.join(ROOT, "_build")
 
 SOURCES = ["runtime.hip", "elementwise.hip", "gemm.hip", "attention.hip", "sampler.hip", "advantage.hip"]
@@ -65,8 +67,14 @@ def build(verbose: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"native benchmark build failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, NATIVE_BENCH)
+    tmp = GEMM_BENCH + ".tmp"
+    cmd = [hipcc(), *COMMON, "-ffp-contract=fast", os.path.join(CSRC, "gemm_bench.hip"), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"GEMM benchmark build failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, GEMM_BENCH)
     if verbose:
-        print(f"built {LIB} and {NATIVE_BENCH}", file=sys.stderr)
+        print(f"built {LIB}, {NATIVE_BENCH} and {GEMM_BENCH}", file=sys.stderr)
     return LIB
 
 

@@ -35,6 +35,217 @@ constexpr int kBufferDword3 = 0x00020000;
 
 DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// ---- direct-to-LDS operand path ----------------------------------------------
+// Operand tiles can also go from memory straight into LDS (buffer_load ... lds, 16 bytes
+// per lane: one wave instruction fills 1 KB, 8 rows of 64 elements), through a ring of S
+// stages: step k + S - 1 is in flight while step k is multiplied, without registers to
+// hold it.  LDS rows are unpadded; the 16-byte chunks of a row are XOR-swizzled so that
+// 16 consecutive rows read at one logical chunk hit 16 distinct 4-bank groups.
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int BM, int BN>
+struct LdsStage {
+    bf16_t a[BM * kBK];
+    bf16_t b[BN * kBK];
+};
+
+DASH_DEV int lds_swizzle(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+// Fill one stage: AI instructions of 8 A rows, then BI of 8 B rows.  kb is the step's
+// byte offset along K; kb >= 2^31 (a step past the end) makes every in-range row read
+// out of range, which returns zeros without touching memory, so every step issues the
+// same instructions (padding rows, out of range already, may wrap to a harmless read).
+template <int AI, int BI, int BM, int BN>
+DASH_DEV void lds_dma_stage(LdsStage<BM, BN>& s, const bf16_t* A, int a_bytes, const bf16_t* W, int w_bytes,
+                            const uint32_t* a_off, const uint32_t* b_off, uint32_t kb, int wave, int wpol) {
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(A), 0, a_bytes, kBufferDword3);
+    const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(W), 0, w_bytes, kBufferDword3);
+#pragma unroll
+    for (int j = 0; j < AI; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)&s.a[(wave * AI + j) * 8 * kBK], 16, a_off[j] + kb, 0, 0,
+                                                 0);
+#pragma unroll
+    for (int j = 0; j < BI; ++j) {
+        if (wpol)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (lds_void*)&s.b[(wave * BI + j) * 8 * kBK], 16, b_off[j] + kb,
+                                                     0, 0, 2);
+        else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (lds_void*)&s.b[(wave * BI + j) * 8 * kBK], 16, b_off[j] + kb,
+                                                     0, 0, 0);
+    }
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (n < 64)
+template <int n>
+DASH_DEV void wait_vmcnt() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14));
+}
+
+// ---- epilogues shared by the GEMM kernels ------------------------------------
+// acc[i * TN + j][r] of a wave holds row (r / 4) * 8 + (lane / 32) * 4 + r % 4 and column
+// lane % 32 of its 32 x 32 block (i, j).
+
+template <int BM, int BN, int WGM, int WGN>
+DASH_DEV void store_f32_epilogue(const f32x16_t* acc, float* Cp, int M, int N, int ldc, int m0, int nt, int lane,
+                                 int wr, int wc) {
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = nt * BN + wc * WN + j * 32 + ccol;
+            if (n >= N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
+                if (m < M) Cp[(size_t)m * ldc + n] = acc[i * TN + j][r];
+            }
+        }
+}
+
+// h = silu(gate) * up: a wave's column blocks hold TN/2 gate blocks, then the TN/2 up
+// blocks of the same columns
+template <int BM, int BN, int WGM, int WGN>
+DASH_DEV void swiglu_epilogue(const f32x16_t* acc, bf16_t* H, int M, int N, int ldc, int m0, int nt, int lane, int wr,
+                              int wc) {
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
+    const int ff = N >> 1;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN / 2; ++j) {
+            const int col = nt * (BN / 2) + wc * (WN / 2) + j * 32 + ccol;
+            if (col >= ff) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
+                if (m < M) H[(size_t)m * ldc + col] = f2bf(silu(acc[i * TN + j][r]) * acc[i * TN + j + TN / 2][r]);
+            }
+        }
+}
+
+// QKV epilogue inputs (fetched before the main loop so that their latency, for the k / v
+// tiles a dependent chain of position and slot, then the page table, hides behind it):
+// per tile row its cache page (or -1) and key within the page (row_page / row_key, LDS);
+// per thread the bias and the RoPE cosines / sines of its pairs.
+template <int BM, int BN, int NT>
+struct QkvPre {
+    static constexpr int kRows = BM * (BN / 2) / NT;  // RoPE pairs per thread
+    static constexpr int kRowsV = BM * BN / NT;       // v elements per thread
+    float2 rope_cs[kRows > 0 ? kRows : 1];
+    float bias_a = 0.f, bias_b = 0.f;
+};
+
+template <int BM, int BN, int NT>
+DASH_DEV void qkv_prefetch(const QkvRopeArgs& qa, int M, int N, int m0, int nt, int tid, int* row_page, int* row_key,
+                           QkvPre<BM, BN, NT>& pre) {
+    static_assert(BN == 128, "the QKV epilogue works on 128-column tiles (whole heads)");
+    static_assert(BM * (BN / 2) % NT == 0 && NT % (BN / 2) == 0, "RoPE pair mapping");
+    static_assert(BM * BN % NT == 0 && NT % BN == 0, "v mapping");
+    const KVGeom& g = qa.g;
+    const int hd = g.head_dim, half = hd >> 1;
+    const int lg_half = hd == 128 ? 6 : 5;  // head_dim is 64 or 128
+    const int n0 = nt * BN;
+    const int q_cols = qa.n_heads * hd, k_end_col = q_cols + g.n_kv * hd;
+    if (n0 >= q_cols && tid < BM) {
+        const int m = m0 + tid;
+        int page = -1, key = 0;
+        if (m < M) {
+            const int p = qa.pos[m];
+            page = kv_page_of(g, qa.page_table, qa.slot[m], p);
+            key = p % g.page_size;
+            if (page < 0 && n0 < k_end_col && qa.status) atomicOr(qa.status, 1u);
+        }
+        row_page[tid] = page;
+        row_key[tid] = key;
+    }
+    if (n0 < k_end_col) {  // q / k tile: thread t takes pair t % (BN/2) of rows t / (BN/2) + u NT / (BN/2)
+        const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
+        const int hl = pi >> lg_half, i = pi & (half - 1);
+        const int n = n0 + hl * hd + i;
+        pre.bias_a = bf2f(qa.bias[n]);
+        pre.bias_b = bf2f(qa.bias[n + half]);
+#pragma unroll
+        for (int u = 0; u < QkvPre<BM, BN, NT>::kRows; ++u) {
+            const int m = min(m0 + r0 + u * (NT / (BN / 2)), M - 1);
+            pre.rope_cs[u] = *reinterpret_cast<const float2*>(qa.cs + ((size_t)m * half + i) * 2);
+        }
+    } else {  // v tile: thread t takes column t % BN of rows t / BN + u NT / BN
+        const int n = n0 + tid % BN;
+        pre.bias_a = n < N ? bf2f(qa.bias[n]) : 0.f;
+    }
+}
+
+// Stage the fp32 tile in LDS (Cs: BM x (BN + 4) floats of LDS that no wave reads any
+// more), then one thread per RoPE pair (q, k tiles) or v element adds the bias, rotates
+// and writes q or the cache slot.
+template <int BM, int BN, int WGM, int WGN>
+DASH_DEV void qkv_epilogue(const f32x16_t* acc, float* Cs, const QkvRopeArgs& qa, int M, int N, int m0, int nt,
+                           int tid, int wr, int wc, const int* row_page, const int* row_key,
+                           const QkvPre<BM, BN, 64 * WGM * WGN>& pre) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    constexpr int CS = BN + 4;
+    constexpr int kRows = QkvPre<BM, BN, NT>::kRows, kRowsV = QkvPre<BM, BN, NT>::kRowsV;
+    const int lane = tid & 63;
+    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                Cs[(wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3)) * CS + wc * WN + j * 32 + ccol] = acc[i * TN + j][r];
+    __syncthreads();
+    const KVGeom& g = qa.g;
+    const int hd = g.head_dim, half = hd >> 1;
+    const int lg_half = hd == 128 ? 6 : 5;
+    const int n0 = nt * BN;
+    const int q_cols = qa.n_heads * hd, k_end = q_cols + g.n_kv * hd;
+    if (n0 < k_end) {
+        const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
+        const int hl = pi >> lg_half, i = pi & (half - 1);
+        const int c = hl * hd + i, n = n0 + c;
+#pragma unroll
+        for (int u = 0; u < kRows; ++u) {
+            const int rl = r0 + u * (NT / (BN / 2)), m = m0 + rl;
+            if (m >= M) continue;
+            const float a = Cs[rl * CS + c] + pre.bias_a;
+            const float b = Cs[rl * CS + c + half] + pre.bias_b;
+            float lo, hi;
+            rope_pair(a, b, pre.rope_cs[u].x, pre.rope_cs[u].y, lo, hi);
+            if (n < q_cols) {
+                bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + n / hd) * hd;
+                q[i] = f2bf(lo);
+                q[i + half] = f2bf(hi);
+            } else if (row_page[rl] >= 0) {
+                bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) / hd, 0);
+                // cache appends are non-temporal stores (see the v append below)
+                __builtin_nontemporal_store(f2bf(lo), &kb[k_index_bf16(g, row_key[rl], i)]);
+                __builtin_nontemporal_store(f2bf(hi), &kb[k_index_bf16(g, row_key[rl], i + half)]);
+            }
+        }
+    } else {
+        const int c = tid % BN, r0 = tid / BN;
+        const int n = n0 + c, jj = n - k_end;
+#pragma unroll
+        for (int u = 0; u < kRowsV; ++u) {
+            const int rl = r0 + u * (NT / BN), m = m0 + rl;
+            if (m >= M || n >= N || row_page[rl] < 0) continue;
+            const float v = Cs[rl * CS + c] + pre.bias_a;
+            bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
+            // A decode step writes one key per row: 2 bytes into each of the 16-byte groups
+            // of 8 keys, lines that later steps read from memory anyway.  Non-temporal
+            // stores keep these partial lines out of L2: measured 8% less QKV time and 2%
+            // less decode-attention time at 1.5B, 1024 sequences.
+            __builtin_nontemporal_store(f2bf(v), &vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))]);
+        }
+    }
+}
+
 // On gfx950 the 32x32x16 bf16 MFMA sustains about twice the rate of 16x16x32
 // (measured: ~2.1 vs ~1.24 PFLOP/s with register-only operands), so the main
 // kernel uses 32 x 32 output blocks.  Operand layout (per 16-wide k-step): lane l
@@ -153,51 +364,10 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
         }
     };
 
-    // QKV epilogue inputs, fetched before the main loop so that their latency (for the
-    // k / v tiles a dependent chain: position and slot, then the page table) hides
-    // behind it: per tile row its cache page (or -1) and key within the page; per
-    // thread the bias and the RoPE cosines / sines of its pairs.
+    // QKV epilogue inputs, fetched before the main loop so that their latency hides behind it
     [[maybe_unused]] __shared__ int row_page[EPI == EPI_QKV_ROPE ? BM : 1], row_key[EPI == EPI_QKV_ROPE ? BM : 1];
-    constexpr int kRows = EPI == EPI_QKV_ROPE ? BM * (BN / 2) / NT : 1;   // RoPE pairs per thread
-    constexpr int kRowsV = EPI == EPI_QKV_ROPE ? BM * BN / NT : 1;        // v elements per thread
-    [[maybe_unused]] float2 rope_cs[kRows];
-    [[maybe_unused]] float bias_a = 0.f, bias_b = 0.f;
-    if constexpr (EPI == EPI_QKV_ROPE) {
-        static_assert(BM * (BN / 2) % NT == 0 && NT % (BN / 2) == 0, "RoPE pair mapping");
-        static_assert(BM * BN % NT == 0 && NT % BN == 0, "v mapping");
-        const KVGeom& g = qa.g;
-        const int hd = g.head_dim, half = hd >> 1;
-        const int lg_half = hd == 128 ? 6 : 5;  // head_dim is 64 or 128
-        const int n0 = nt * BN;
-        const int q_cols = qa.n_heads * hd, k_end_col = q_cols + g.n_kv * hd;
-        if (n0 >= q_cols && tid < BM) {
-            const int m = m0 + tid;
-            int page = -1, key = 0;
-            if (m < M) {
-                const int p = qa.pos[m];
-                page = kv_page_of(g, qa.page_table, qa.slot[m], p);
-                key = p % g.page_size;
-                if (page < 0 && n0 < k_end_col && qa.status) atomicOr(qa.status, 1u);
-            }
-            row_page[tid] = page;
-            row_key[tid] = key;
-        }
-        if (n0 < k_end_col) {  // q / k tile: thread t takes pair t % (BN/2) of rows t / (BN/2) + u NT / (BN/2)
-            const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
-            const int hl = pi >> lg_half, i = pi & (half - 1);
-            const int n = n0 + hl * hd + i;
-            bias_a = bf2f(qa.bias[n]);
-            bias_b = bf2f(qa.bias[n + half]);
-#pragma unroll
-            for (int u = 0; u < kRows; ++u) {
-                const int m = min(m0 + r0 + u * (NT / (BN / 2)), M - 1);
-                rope_cs[u] = *reinterpret_cast<const float2*>(qa.cs + ((size_t)m * half + i) * 2);
-            }
-        } else {  // v tile: thread t takes column t % BN of rows t / BN + u NT / BN
-            const int n = n0 + tid % BN;
-            bias_a = n < N ? bf2f(qa.bias[n]) : 0.f;
-        }
-    }
+    [[maybe_unused]] QkvPre<BM, BN, NT> pre;
+    if constexpr (EPI == EPI_QKV_ROPE) qkv_prefetch<BM, BN, NT>(qa, M, N, m0, nt, tid, row_page, row_key, pre);
 
     const int n_k = (k_end - k_begin + kBK - 1) / kBK;
 #pragma unroll
@@ -216,97 +386,176 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
         }
     }
 
-    // acc[i][j][r]: row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j)
-    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
     if constexpr (EPI == EPI_QKV_ROPE) {
-        // Stage the fp32 tile in LDS (the operand tiles are dead after the loop's last
-        // barrier), then one thread per RoPE pair (q, k tiles) or v element.
-        constexpr int CS = BN + 4;
-        static_assert(BM * CS * 4 <= (int)sizeof(Bs), "C tile must fit the B operand LDS");
-        float* Cs = reinterpret_cast<float*>(&Bs[0][0]);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    Cs[(wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3)) * CS + wc * WN + j * 32 + ccol] = acc[i][j][r];
-        __syncthreads();
-        const KVGeom& g = qa.g;
-        const int hd = g.head_dim, half = hd >> 1;
-        const int lg_half = hd == 128 ? 6 : 5;
-        const int n0 = nt * BN;
-        const int q_cols = qa.n_heads * hd, k_end = q_cols + g.n_kv * hd;
-        if (n0 < k_end) {
-            const int pi = tid % (BN / 2), r0 = tid / (BN / 2);
-            const int hl = pi >> lg_half, i = pi & (half - 1);
-            const int c = hl * hd + i, n = n0 + c;
-#pragma unroll
-            for (int u = 0; u < kRows; ++u) {
-                const int rl = r0 + u * (NT / (BN / 2)), m = m0 + rl;
-                if (m >= M) continue;
-                const float a = Cs[rl * CS + c] + bias_a;
-                const float b = Cs[rl * CS + c + half] + bias_b;
-                float lo, hi;
-                rope_pair(a, b, rope_cs[u].x, rope_cs[u].y, lo, hi);
-                if (n < q_cols) {
-                    bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + n / hd) * hd;
-                    q[i] = f2bf(lo);
-                    q[i + half] = f2bf(hi);
-                } else if (row_page[rl] >= 0) {
-                    bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) / hd, 0);
-                    // cache appends are non-temporal stores (see the v append below)
-                    __builtin_nontemporal_store(f2bf(lo), &kb[k_index_bf16(g, row_key[rl], i)]);
-                    __builtin_nontemporal_store(f2bf(hi), &kb[k_index_bf16(g, row_key[rl], i + half)]);
-                }
-            }
-        } else {
-            const int c = tid % BN, r0 = tid / BN;
-            const int n = n0 + c, jj = n - k_end;
-#pragma unroll
-            for (int u = 0; u < kRowsV; ++u) {
-                const int rl = r0 + u * (NT / BN), m = m0 + rl;
-                if (m >= M || n >= N || row_page[rl] < 0) continue;
-                const float v = Cs[rl * CS + c] + bias_a;
-                bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
-                // A decode step writes one key per row: 2 bytes into each of the 16-byte groups
-                // of 8 keys, lines that later steps read from memory anyway.  Non-temporal
-                // stores keep these partial lines out of L2: measured 8% less QKV time and 2%
-                // less decode-attention time at 1.5B, 1024 sequences.
-                __builtin_nontemporal_store(f2bf(v), &vb[v_index_bf16(g, row_key[rl], jj & (hd - 1))]);
-            }
-        }
+        // the fp32 tile is staged in the B operand LDS (dead after the loop's last barrier)
+        static_assert(BM * (BN + 4) * 4 <= (int)sizeof(Bs), "C tile must fit the B operand LDS");
+        qkv_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<float*>(&Bs[0][0]), qa, M, N, m0, nt, tid, wr, wc,
+                                       row_page, row_key, pre);
     } else if constexpr (EPI == EPI_STORE_F32) {
-        float* Cp = reinterpret_cast<float*>(C) + split * split_stride;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = nt * BN + wc * WN + j * 32 + ccol;
-                if (n >= N) continue;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
-                    if (m < M) Cp[(size_t)m * ldc + n] = acc[i][j][r];
-                }
-            }
+        store_f32_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<float*>(C) + split * split_stride, M, N, ldc,
+                                             m0, nt, lane, wr, wc);
     } else {
         static_assert(EPI == EPI_SWIGLU, "unknown epilogue");
-        bf16_t* H = reinterpret_cast<bf16_t*>(C);
-        const int ff = N >> 1;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN / 2; ++j) {
-                const int col = nt * (BN / 2) + wc * (WN / 2) + j * 32 + ccol;
-                if (col >= ff) continue;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int m = m0 + wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
-                    if (m < M) H[(size_t)m * ldc + col] = f2bf(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
-                }
-            }
+        swiglu_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<bf16_t*>(C), M, N, ldc, m0, nt, lane, wr, wc);
     }
+}
+
+// The same product with the direct-to-LDS operand path: S LDS stages, one barrier per
+// k-step.  At step k a wave waits until its own part of step k has landed, the barrier
+// then guarantees every wave's part (and that every wave is done with step k - 1), the
+// stage of step k - 1 is refilled with step k + S - 1, and step k is multiplied.  Each
+// stage is its own LDS variable, so the compiler lets the loads of the other stages stay
+// in flight while a stage is read.  Same fragments, same MFMA order as gemm_bf16_k:
+// identical results.  Measured on the 1.5B decode shapes at 1024 rows (weights cold):
+// the output projection 14.7 -> 10.6 us, the QKV projection 15.5 -> 11.5 us with
+// 128 x 64 tiles; gate/up, down and the LM head gain nothing (their per-CU rate stays
+// at ~30% of the MFMA peak either way), so they keep gemm_bf16_k.
+template <int BM, int BN, int WGM, int WGN, int S, int EPI, int WPOL = 0>
+__global__ void __launch_bounds__(64 * WGM * WGN)
+gemm_lds_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __restrict__ C, int M, int N, int K,
+           int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride, QkvRopeArgs qa) {
+    constexpr int NT = 64 * WGM * WGN, NW = WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    constexpr int AI = BM / 8 / NW, BI = BN / 8 / NW;  // 1 KB load instructions per wave per k-step
+    constexpr int DPS = AI + BI;
+    static_assert(AI >= 1 && BI >= 1 && BM / 8 % NW == 0 && BN / 8 % NW == 0, "load split");
+    static_assert(S >= 3 && S <= 4, "stages");
+    static_assert(TM >= 1 && TN >= 1, "wave tile smaller than one MFMA block");
+    static_assert(EPI == EPI_STORE_F32 || EPI == EPI_QKV_ROPE, "epilogue");
+    __shared__ __attribute__((aligned(1024))) LdsStage<BM, BN> st0;
+    __shared__ __attribute__((aligned(1024))) LdsStage<BM, BN> st1;
+    __shared__ __attribute__((aligned(1024))) LdsStage<BM, BN> st2;
+    __shared__ __attribute__((aligned(1024))) LdsStage<(S > 3 ? BM : 8), (S > 3 ? BN : 8)> st3;
+
+    const int w = xcd_remap(blockIdx.x, gridDim.x);
+    const int mt = w % m_tiles;
+    const int rest = w / m_tiles;
+    const int nt = rest % n_tiles;
+    const int split = rest / n_tiles;
+    const int m0 = mt * BM;
+    const int k_begin = split * kps;
+    const int k_end = min(K, k_begin + kps);
+    const int n_k = (k_end - k_begin) / kBK;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = wave / WGN, wc = wave % WGN;
+    const int a_bytes = (int)((size_t)M * K * 2), w_bytes = (int)((size_t)N * K * 2);
+
+    // lane l of load instruction j fills LDS chunk l % 8 of row l / 8 of its 8-row group:
+    // it loads the logical chunk that the swizzle puts there
+    constexpr uint32_t kOut = 0x80000000u;
+    uint32_t a_off[AI], b_off[BI];
+#pragma unroll
+    for (int j = 0; j < AI; ++j) {
+        const int row = (wave * AI + j) * 8 + (lane >> 3);
+        const int m = m0 + row;
+        a_off[j] = m < M ? (uint32_t)(((size_t)m * K + k_begin + lds_swizzle(row, lane & 7) * 8) * 2) : kOut;
+    }
+#pragma unroll
+    for (int j = 0; j < BI; ++j) {
+        const int row = (wave * BI + j) * 8 + (lane >> 3);
+        const int n = nt * BN + row;
+        b_off[j] = n < N ? (uint32_t)(((size_t)n * K + k_begin + lds_swizzle(row, lane & 7) * 8) * 2) : kOut;
+    }
+
+    [[maybe_unused]] __shared__ int row_page[EPI == EPI_QKV_ROPE ? BM : 1], row_key[EPI == EPI_QKV_ROPE ? BM : 1];
+    [[maybe_unused]] QkvPre<BM, BN, NT> pre;
+    if constexpr (EPI == EPI_QKV_ROPE) qkv_prefetch<BM, BN, NT>(qa, M, N, m0, nt, tid, row_page, row_key, pre);
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int frow = lane & 31, fhalf = lane >> 5;
+    auto compute = [&](const LdsStage<BM, BN>& sg) {
+#pragma unroll
+        for (int ks = 0; ks < kBK / 16; ++ks) {
+            bf16x8_t af[TM], bfr[TN];
+            const int c = ks * 2 + fhalf;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int row = wr * WM + i * 32 + frow;
+                af[i] = *reinterpret_cast<const bf16x8_t*>(&sg.a[row * kBK + (lds_swizzle(row, c) << 3)]);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int row = wc * WN + j * 32 + frow;
+                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&sg.b[row * kBK + (lds_swizzle(row, c) << 3)]);
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
+    };
+    auto stage = [&](int i) -> LdsStage<BM, BN>& {
+        if (i == 0) return st0;
+        if (i == 1) return st1;
+        if constexpr (S > 3) {
+            if (i == 3) return st3;
+        }
+        return st2;
+    };
+    auto step_bytes = [&](int k) { return k < n_k ? (uint32_t)k * kBK * 2 : 0x80000000u; };
+#pragma unroll
+    for (int p = 0; p < S - 1; ++p)
+        lds_dma_stage<AI, BI>(stage(p), A, a_bytes, W, w_bytes, a_off, b_off, step_bytes(p), wave, WPOL);
+    // one k-step from stage ST (the stage index is a constant in every expansion)
+#define DASH_LDS_STEP(ST, KK)                                                                               \
+    do {                                                                                                   \
+        const int k_ = (KK);                                                                               \
+        wait_vmcnt<(S - 2) * DPS>();                                                                       \
+        __builtin_amdgcn_s_barrier();                                                                      \
+        lds_dma_stage<AI, BI>(stage(((ST) + S - 1) % S), A, a_bytes, W, w_bytes, a_off, b_off,              \
+                              step_bytes(k_ + S - 1), wave, WPOL);                                         \
+        compute(stage(ST));                                                                                \
+    } while (0)
+    int k = 0;
+    for (; k + S <= n_k; k += S) {
+        DASH_LDS_STEP(0, k);
+        DASH_LDS_STEP(1, k + 1);
+        DASH_LDS_STEP(2, k + 2);
+        if constexpr (S > 3) DASH_LDS_STEP(3, k + 3);
+    }
+    if (k < n_k) DASH_LDS_STEP(0, k++);
+    if (k < n_k) DASH_LDS_STEP(1, k++);
+    if constexpr (S > 3) {
+        if (k < n_k) DASH_LDS_STEP(2, k++);
+    }
+#undef DASH_LDS_STEP
+
+    if constexpr (EPI == EPI_QKV_ROPE) {
+        // the fp32 tile is staged in LDS of its own (a stage is too small for it)
+        __shared__ __attribute__((aligned(16))) float cstage[BM * (BN + 4)];
+        wait_vmcnt<0>();  // the out-of-range loads of the steps past the end still write their stage
+        qkv_epilogue<BM, BN, WGM, WGN>(&acc[0][0], cstage, qa, M, N, m0, nt, tid, wr, wc, row_page, row_key, pre);
+    } else {
+        store_f32_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<float*>(C) + split * split_stride, M, N, ldc,
+                                             m0, nt, lane, wr, wc);
+        wait_vmcnt<0>();  // the out-of-range loads of the steps past the end still write their stage
+    }
+}
+
+template <int BM, int BN, int WGM, int WGN, int S, int EPI, int WPOL = 0>
+hipError_t run_lds(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int nsplit,
+                   size_t split_stride, hipStream_t st, const QkvRopeArgs& qa = QkvRopeArgs{}) {
+    const int m_tiles = (M + BM - 1) / BM;
+    const int n_tiles = (N + BN - 1) / BN;
+    int kps = K;
+    if (nsplit > 1) {
+        kps = (K + nsplit - 1) / nsplit;
+        kps = (kps + kBK - 1) / kBK * kBK;
+    }
+    if ((K + kps - 1) / kps != nsplit) return hipErrorInvalidValue;
+    if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
+    gemm_lds_k<BM, BN, WGM, WGN, S, EPI, WPOL><<<m_tiles * n_tiles * nsplit, 64 * WGM * WGN, 0, st>>>(
+        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride, qa);
+    return hipGetLastError();
 }
 
 template <int BM, int BN, int WGM, int WGN, int PD, int EPI, int WPOL = 0>
@@ -464,6 +713,17 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             if (M <= 128)  // measured 10-18% faster than 256x256 at 96-128 rows
                 return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+        }
+        if (K < 4096 && M >= 256 && M <= 4096) {
+            // Unsplit short reductions (the output projection; QKV where it is not fused):
+            // the direct-to-LDS kernel, on the largest tile that still gives the launch
+            // about 160 or more work-groups.  Measured on the 0.5B, 1.5B and 3B shapes at
+            // 256-2048 rows (dash_gemm_bench, weights cold): 7-36% faster than the
+            // register-staged tiles (1.5B at 1024 rows: 14.8 -> 10.5 us).
+            if (M <= 512) return run_lds<64, 64, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            if (M <= 1024 || (long)(M / 128) * ((N + 127) / 128) < 160)
+                return run_lds<128, 64, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
         }
         if (M <= 256 && (K < 4096 || M <= 64)) {
             // Few work-groups stream the weights here; four k-steps in flight per thread
