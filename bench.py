@@ -28,9 +28,9 @@ BF16_PEAK_TFLOPS = 2500.0
 # 617.3 MB read + 3.15 MB written), valid for the attention sources it was measured with.
 ATTN_TRAFFIC = {
     "workload": "1.5b-b1024",
-    "bytes_per_launch": 620_400_000,
+    "bytes_per_launch": 621_200_000,
     "sources": {
-        "paper_2505_17218_amd/csrc/attention.hip": "c19255d25be67b74a9195558521f1ee6bb07db198c4e556d9aa60ea2079b474e",
+        "paper_2505_17218_amd/csrc/attention.hip": "88aa7d45041ab5c45850e89d3787c6047d23e157e7d794e886967242728225db",
         "paper_2505_17218_amd/csrc/common.h": "16d56f2b1c378ddeb1902011b1b9beb198deb192709a5250858858f49c6d4547",
     },
 }
