@@ -272,13 +272,16 @@ int dash_decode_step_noalloc(dash_model* model, dash_kv* kv, const int32_t* d_to
 
 /*
  * dash_decode_step for a batch made of prefix-sharing groups (the G samples of a
- * prompt after the group fork): rows d_group_off[i] .. d_group_off[i+1]-1 (int32
- * device array of n_groups + 1 ascending offsets, the last equal to n_rows, each
- * group at most group_size <= 8 rows) share their first shared_len positions, i.e.
- * the same pages (shared_len a multiple of page_size, at most the prompt's full
- * pages).  Decode attention then reads each shared page once per group instead of
- * once per row.  Results are bit-identical to dash_decode_step.  DASH_ENOTSUP for
- * group_size > 8; fp32 models run the ungrouped kernels.
+ * prompt after the group fork, Sec. 3.4): rows d_group_off[i] .. d_group_off[i+1]-1
+ * (int32 device array of n_groups + 1 ascending offsets, the first 0 and the last
+ * equal to n_rows, each group at most group_size <= 8 rows) share their first
+ * shared_len positions, i.e. the same pages (shared_len a multiple of page_size, at
+ * most max_ctx and at most the prompt's full pages).  Decode attention then runs
+ * those shared pages once per group and kv head, for all the group's query heads
+ * at once, and continues every row from the online-softmax state this leaves
+ * (kept in the workspace) over its own pages.  Results are bit-identical to
+ * dash_decode_step.  DASH_ENOTSUP for group_size > 8; fp32 models, and shapes the
+ * prefix kernel does not cover, run the per-row kernel (same results).
  */
 int dash_decode_step_grouped(dash_model* model, dash_kv* kv, const int32_t* d_tokens, const int32_t* d_slots,
                              const int32_t* d_pos, int32_t n_rows, const int32_t* d_group_off, int32_t n_groups,

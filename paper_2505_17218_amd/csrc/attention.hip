@@ -40,7 +40,13 @@ constexpr int kBufferDword3 = 0x00020000;  // raw buffer resource word 3 (gfx9 f
 // Prefill keeps the default: each key block is read again by every 16-query column
 // block of its sequence and should stay cached (streaming it measured 1.75x slower).
 constexpr int kKvStream = 2, kKvReuse = 0;
-constexpr int kMaxGroupWaves = 16;  // samples per group served by one workgroup
+
+// s_waitcnt vmcnt(n), the other counters left alone (gfx9 encoding, n < 64)
+template <int n>
+DASH_DEV void vm_wait() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14));
+}
 
 // ---- shared MFMA block step ---------------------------------------------
 // A wave attends 16 "columns" (decode: the query heads of one GQA group;
@@ -180,15 +186,44 @@ DASH_DEV void attn_store(const AttnState<HD>& st, float l, bf16_t* orow, int grp
     }
 }
 
-// ---- decode ----------------------------------------------------------------
+// The online-softmax state of one column in memory (kPrefixStateStride<HD> floats per
+// row and query head): the accumulators in the partial layout (dims d*16 + grp*4 ..
+// +4), then each lane group's partial denominator, then the running max.  Storing and
+// reloading it moves the exact register values, so a chain continued from it gives
+// the same bits as one run through.
+template <int HD>
+constexpr int kPrefixStateStride = HD + 8;
 
 template <int HD>
+DASH_DEV void attn_state_store(const AttnState<HD>& st, float* sp, int grp) {
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d)
+        *reinterpret_cast<float4*>(sp + d * 16 + grp * 4) = make_float4(st.acc[d][0], st.acc[d][1], st.acc[d][2], st.acc[d][3]);
+    sp[HD + grp] = st.l;
+    if (grp == 0) sp[HD + 4] = st.m;
+}
+
+template <int HD>
+DASH_DEV void attn_state_load(AttnState<HD>& st, const float* sp, int grp) {
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+        const float4 v = *reinterpret_cast<const float4*>(sp + d * 16 + grp * 4);
+        st.acc[d] = f32x4_t{v.x, v.y, v.z, v.w};
+    }
+    st.l = sp[HD + grp];
+    st.m = sp[HD + 4];
+}
+
+// ---- decode ----------------------------------------------------------------
+
+template <int HD, bool PRE = false>
 __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
                                                          const int32_t* __restrict__ slot,
                                                          const int32_t* __restrict__ page_table,
                                                          const bf16_t* __restrict__ pool, KVGeom g, int layer,
                                                          int n_heads, bf16_t* __restrict__ o, int max_splits,
-                                                         float* __restrict__ part, float scale_log2) {
+                                                         float* __restrict__ part, float scale_log2,
+                                                         const float* __restrict__ pre_state, int pre_blocks) {
     constexpr int NC = HD / 32;
     constexpr int ND = HD / 16;
     const int lane = threadIdx.x;
@@ -208,7 +243,7 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
     const int per = g.split_keys >> 5;  // key blocks per split
     const int nsplit = min((nblk + per - 1) / per, max_splits);  // rows past max_ctx are not valid input
     if (split >= nsplit) return;
-    const int b_begin = split * per;
+    int b_begin = split * per;
     const int b_end = min(nblk, b_begin + per);
 
     // Q^T operand per 32-dim chunk: lane holds q[head][c*32 + grp*8 .. +8] (zero for padding heads).
@@ -223,6 +258,12 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
     }
     AttnState<HD> st;
     attn_init(st);
+    if (PRE && split == 0 && pre_blocks > 0) {
+        // the row's first pre_blocks blocks (its group's shared prompt pages) were run by
+        // decode_attn_prefix_k: continue the chain from the state it left
+        if (head < rep) attn_state_load<HD>(st, pre_state + ((size_t)row * n_heads + kvh * rep + head) * kPrefixStateStride<HD>, grp);
+        b_begin = pre_blocks;
+    }
     // two register sets: block b + 1 is fetched while block b is multiplied
     KVRegs<HD> r[2];
     auto fetch = [&](KVRegs<HD>& dst, int b) {
@@ -237,13 +278,15 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
         else
             load_kv<HD, kKvStream>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
     };
-    fetch(r[0], b_begin);
-    for (int b = b_begin; b < b_end; b += 2) {
-        fetch(r[1], min(b + 1, b_end - 1));
-        attn_block<HD>(st, r[0], qf, b << 5, ctx, ctx, scale_log2, grp);
-        if (b + 1 >= b_end) break;
-        fetch(r[0], min(b + 2, b_end - 1));
-        attn_block<HD>(st, r[1], qf, (b + 1) << 5, ctx, ctx, scale_log2, grp);
+    if (b_begin < b_end) {
+        fetch(r[0], b_begin);
+        for (int b = b_begin; b < b_end; b += 2) {
+            fetch(r[1], min(b + 1, b_end - 1));
+            attn_block<HD>(st, r[0], qf, b << 5, ctx, ctx, scale_log2, grp);
+            if (b + 1 >= b_end) break;
+            fetch(r[0], min(b + 2, b_end - 1));
+            attn_block<HD>(st, r[1], qf, (b + 1) << 5, ctx, ctx, scale_log2, grp);
+        }
     }
     const float l = attn_denominator(st);
     if (head >= rep) return;
@@ -266,161 +309,99 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
 }
 
 // ---- decode, prefix-shared groups --------------------------------------------
-// The G samples of a prompt share the prompt's full pages (the group fork).  One
-// workgroup serves a whole group for one kv head and one context split: wave w
-// handles batch row off[g] + w.  Key blocks inside the shared prefix are fetched
-// once per workgroup (each wave loads a share of the block's 16-byte fragments,
-// staged through LDS in fragment order so every wave then reads whole fragments
-// with conflict-free 16-byte LDS reads); blocks past the prefix are streamed by
-// each wave from its own pages exactly as in the per-row kernel.  Per row the
-// blocks, the arithmetic and its order are those of decode_attn_bf16_k, so the
-// results are bit-identical to it.
+// The G samples of a prompt share the prompt's full pages (the group fork), and for
+// every query column the per-row chain above starts with those shared blocks.  This
+// kernel runs that first part of the chain once per (group, kv head) for all the
+// group's query columns, G x rep of them in tiles of 16, one wave per tile, with the
+// group's shared pages fetched once into LDS (whole pages, copied verbatim by
+// direct-to-LDS loads, so a lane's fragment sits at the same offset as in memory);
+// it leaves each column's state for decode_attn_bf16_k, which continues every row over
+// its own blocks.  Per column the blocks, the arithmetic and its order are those of
+// the per-row chain, so the results are bit-identical to decode_attn_bf16_k alone.
+// Column c of group [r0, r1) is row r0 + c / rep, query head kvh * rep + c % rep.
+// Pages go through LDS in chunks of kPrefixLdsBytes (all of a 256-key prompt's pages
+// at head dim 128 and page size 32).
+constexpr int kPrefixLdsBytes = 128 * 1024;
 
-template <int HD, int NW>
-__global__ void __launch_bounds__(64 * NW)
-decode_attn_group_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
-                         const int32_t* __restrict__ slot, const int32_t* __restrict__ page_table,
-                         const bf16_t* __restrict__ pool, KVGeom g, int layer, int n_heads,
-                         const int32_t* __restrict__ group_off, int shared_len, bf16_t* __restrict__ o,
-                         int max_splits, float* __restrict__ part, float scale_log2) {
+template <int HD>
+__global__ void __launch_bounds__(512) decode_attn_prefix_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
+                                                            const int32_t* __restrict__ slot,
+                                                            const int32_t* __restrict__ page_table,
+                                                            const bf16_t* __restrict__ pool, KVGeom g, int layer,
+                                                            int n_heads, const int32_t* __restrict__ group_off,
+                                                            int pre_blocks, float* __restrict__ state, float scale_log2) {
     constexpr int NC = HD / 32, ND = HD / 16;
-    constexpr int NF = 2 * NC + ND;  // 1 KB fragments per 32-key block (K halves x chunks, then V blocks)
-    __shared__ uint4 lds[2][NF * 64];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    __shared__ __attribute__((aligned(1024))) char lds[kPrefixLdsBytes];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nw = blockDim.x >> 6;
     const int n_kv = g.n_kv;
-    const int grp_id = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv, split = blockIdx.y;
-    const int r0 = group_off[grp_id], r1 = group_off[grp_id + 1];
-    const bool active = w < r1 - r0;
-    const int row = active ? r0 + w : r0;
+    const int gi = blockIdx.x / n_kv, kvh = blockIdx.x % n_kv;
+    const int r0 = group_off[gi], r1 = group_off[gi + 1];
+    if (r1 <= r0) return;  // uniform over the workgroup
     const int rep = n_heads / n_kv;
     const int head = lane & 15, grp = lane >> 4;
+    const int c = w * 16 + head;  // this lane's column
+    const bool valid = c < (r1 - r0) * rep;
+    const int row = valid ? r0 + c / rep : r0;
+    const int qh = kvh * rep + (valid ? c % rep : 0);
     const int ctx = pos[row] + 1;
-    // the workgroup walks the blocks of its longest row; shorter rows mask the rest
-    int ctx_max = 0;
-    for (int i = r0; i < r1; ++i) ctx_max = max(ctx_max, pos[i] + 1);
-    const int per = g.split_keys >> 5;
-    const int nblk_wg = (ctx_max + 31) >> 5;
-    const int nsplit_wg = min((nblk_wg + per - 1) / per, max_splits);
-    if (split >= nsplit_wg) return;  // uniform over the workgroup
-    const int nblk = (ctx + 31) >> 5;
-    const int nsplit = min((nblk + per - 1) / per, max_splits);
-    const int b_begin = split * per;
-    const int b_end_wg = min(nblk_wg, b_begin + per);
-    const int b_end = min(nblk, b_begin + per);
-    const int sh_blocks = min(shared_len >> 5, b_end_wg);  // blocks [0, sh_blocks) are shared
-    const int sl0 = slot[r0], sl = slot[row];
 
     bf16x8_t qf[NC];
     {
-        const bf16_t* qrow = q + ((size_t)row * n_heads + kvh * rep + (head < rep ? head : 0)) * HD;
+        const bf16_t* qrow = q + ((size_t)row * n_heads + qh) * HD;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            uint4 v = head < rep ? *reinterpret_cast<const uint4*>(qrow + c * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
-            qf[c] = __builtin_bit_cast(bf16x8_t, v);
+        for (int i = 0; i < NC; ++i) {
+            uint4 v = valid ? *reinterpret_cast<const uint4*>(qrow + i * 32 + grp * 8) : make_uint4(0, 0, 0, 0);
+            qf[i] = __builtin_bit_cast(bf16x8_t, v);
         }
     }
     AttnState<HD> st;
     attn_init(st);
 
-    // ---- shared blocks: cooperative fetch through LDS (all waves take part) ----
-    const int bs0 = b_begin, bs1 = min(sh_blocks, b_end_wg);
-    if (bs0 < bs1) {
-        // fragment f of block b: f < 2*NC is K (half f / NC, chunk f % NC), else V block f - 2*NC
-        auto frag_load = [&](int b, int f) -> uint4 {
-            const int key0 = b << 5;
-            int page = kv_page_of(g, page_table, sl0, key0);
+    const int ps = g.page_size;
+    const int blk_bytes = ps * HD * 2;        // a page's K (or V) block
+    const int units = blk_bytes >> 10;        // 1 KB copies per block
+    const int ppc = kPrefixLdsBytes / (2 * blk_bytes);  // pages per LDS chunk (>= 1, checked by the launcher)
+    const int bpp = ps >> 5;                  // 32-key blocks per page
+    const int n_pages = pre_blocks / bpp;
+    const int sl0 = slot[r0];
+    for (int p0 = 0; p0 < n_pages; p0 += ppc) {
+        const int np = min(ppc, n_pages - p0);
+        // copy: unit u = (page j, kind, 1 KB piece) lands at LDS (2 j + kind) * blk_bytes + piece * 1 KB
+        int issued = 0;
+        for (int u = w; u < np * 2 * units; u += nw) {
+            const int j = u / (2 * units), kind = (u / units) & 1, piece = u % units;
+            int page = kv_page_of(g, page_table, sl0, (p0 + j) * ps);
             const bool ok = page >= 0;
             page = ok ? page : 0;
-            const int kin = key0 % g.page_size;
-            const int bytes = ok ? g.page_size * HD * 2 : 0;
-            if (f < 2 * NC) {
-                const int h = f / NC, c = f % NC;
-                const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-                    const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, 0)), 0, bytes, kBufferDword3);
-                return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                    rk, (((c * g.page_size + kin + h * 16 + head) * 32 + grp * 8) * 2), 0, 0));
-            }
-            const int d = f - 2 * NC;
-            const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-                const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, 1)), 0, bytes, kBufferDword3);
-            return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                rv, ((((kin >> 5) * 4 + grp) * HD + d * 16 + head) * 8) * 2, 0, 0));
-        };
-        constexpr int FPW = (NF + NW - 1) / NW;  // fragments per wave
-        uint4 stage[FPW];
-        auto fetch = [&](int b) {
-#pragma unroll
-            for (int i = 0; i < FPW; ++i)
-                if (w + i * NW < NF) stage[i] = frag_load(b, w + i * NW);
-        };
-        auto put = [&](int buf) {
-#pragma unroll
-            for (int i = 0; i < FPW; ++i)
-                if (w + i * NW < NF) lds[buf][(w + i * NW) * 64 + lane] = stage[i];
-        };
-        fetch(bs0);
-        put(0);
-        __syncthreads();
-        for (int b = bs0; b < bs1; ++b) {
-            const int buf = (b - bs0) & 1;
-            fetch(min(b + 1, bs1 - 1));
-            if (active && b < b_end) {
-                KVRegs<HD> r;
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) r.k[h][c] = lds[buf][(h * NC + c) * 64 + lane];
-#pragma unroll
-                for (int d = 0; d < ND; ++d) r.v[d] = lds[buf][(2 * NC + d) * 64 + lane];
-                attn_block<HD>(st, r, qf, b << 5, ctx, ctx, scale_log2, grp);
-            }
-            if (b + 1 < bs1) put(buf ^ 1);
-            __syncthreads();
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<bf16_t*>(pool + kv_block(g, layer, page, kvh, kind)), 0, ok ? blk_bytes : 0, kBufferDword3);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void*)(lds + (2 * j + kind) * blk_bytes + piece * 1024), 16,
+                piece * 1024 + lane * 16, 0, 0, 0);
+            if ((++issued & 15) == 0) vm_wait<32>();  // at most 48 copies in flight per wave
         }
-    }
-
-    // ---- private blocks: each wave streams its own row ----
-    if (active) {
-        const int bp0 = max(b_begin, bs1);
-        if (bp0 < b_end) {
-            KVRegs<HD> r[2];
-            auto fetch = [&](KVRegs<HD>& dst, int b) {
-                const int key0 = b << 5;
-                int page = kv_page_of(g, page_table, sl, key0);
-                const bool ok = page >= 0;
-                page = ok ? page : 0;
-                load_kv<HD, kKvStream>(dst, pool + kv_block(g, layer, page, kvh, 0),
-                                       pool + kv_block(g, layer, page, kvh, 1), g.page_size, key0 % g.page_size, ok,
-                                       head, grp);
-            };
-            fetch(r[0], bp0);
-            for (int b = bp0; b < b_end; b += 2) {
-                fetch(r[1], min(b + 1, b_end - 1));
-                attn_block<HD>(st, r[0], qf, b << 5, ctx, ctx, scale_log2, grp);
-                if (b + 1 >= b_end) break;
-                fetch(r[0], min(b + 2, b_end - 1));
-                attn_block<HD>(st, r[1], qf, (b + 1) << 5, ctx, ctx, scale_log2, grp);
-            }
-        }
-    }
-    const float l = attn_denominator(st);
-    if (!active || head >= rep || split >= nsplit) return;
-    const int qh = kvh * rep + head;
-    if (nsplit == 1) {
-        attn_store<HD>(st, l, o + ((size_t)row * n_heads + qh) * HD, grp);
-    } else {
-        const size_t base = ((size_t)row * n_heads + qh) * max_splits + split;
-        float* op = part + base * HD;
+        vm_wait<0>();     // this wave's copies have landed
+        __syncthreads();                     // and every other wave's
+        for (int b = p0 * bpp; b < (p0 + np) * bpp; ++b) {
+            const int j = b / bpp - p0, kin = (b % bpp) << 5;
+            const char* kb = lds + (2 * j) * blk_bytes;
+            const char* vb = kb + blk_bytes;
+            KVRegs<HD> r;
 #pragma unroll
-        for (int d = 0; d < ND; ++d)
-            *reinterpret_cast<float4*>(op + d * 16 + grp * 4) =
-                make_float4(st.acc[d][0], st.acc[d][1], st.acc[d][2], st.acc[d][3]);
-        if (grp == 0) {
-            float* ml = part + (size_t)group_off[gridDim.x / n_kv] * n_heads * max_splits * HD + base * 2;
-            ml[0] = st.m;
-            ml[1] = l;
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int i = 0; i < NC; ++i)
+                    r.k[h][i] = *reinterpret_cast<const uint4*>(kb + ((i * ps + kin + h * 16 + head) * 32 + grp * 8) * 2);
+#pragma unroll
+            for (int d = 0; d < ND; ++d)
+                r.v[d] = *reinterpret_cast<const uint4*>(vb + ((((kin >> 5) * 4 + grp) * HD + d * 16 + head) * 8) * 2);
+            attn_block<HD>(st, r, qf, b << 5, ctx, ctx, scale_log2, grp);
         }
+        __syncthreads();  // the chunk's LDS is refilled next
     }
+    if (valid) attn_state_store<HD>(st, state + ((size_t)row * n_heads + qh) * kPrefixStateStride<HD>, grp);
 }
 
 // ---- prefill ---------------------------------------------------------------
@@ -637,10 +618,10 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
         const float sl2 = scale * kLog2e;
         if (g.head_dim == 128)
             decode_attn_bf16_k<128><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
-                                                          g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2);
+                                                          g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2, nullptr, 0);
         else if (g.head_dim == 64)
             decode_attn_bf16_k<64><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
-                                                         g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2);
+                                                         g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2, nullptr, 0);
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
@@ -651,33 +632,46 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
     return hipGetLastError();
 }
 
+bool decode_attention_prefix_ok(const KVGeom& g, int n_heads, int group_size, int shared_len) {
+    const int blk_bytes = g.page_size * g.head_dim * 2;
+    return (g.head_dim == 64 || g.head_dim == 128) && g.page_size % 32 == 0 && blk_bytes % 1024 == 0 &&
+           2 * blk_bytes <= kPrefixLdsBytes && shared_len >= g.page_size && g.split_keys >= g.page_size &&
+           group_size >= 1 && ((long)group_size * (n_heads / g.n_kv) + 15) / 16 <= 8;
+}
+
+size_t decode_attention_prefix_state_bytes(int rows, int n_heads, int head_dim) {
+    return (size_t)rows * n_heads * (head_dim + 8) * 4;
+}
+
 hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, const int32_t* slot,
                                            const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                            int n_heads, const int32_t* group_off, int n_groups, int group_size,
                                            int shared_len, void* o, int rows, int max_ctx, float* ws_part,
-                                           hipStream_t st) {
+                                           float* ws_state, hipStream_t st) {
     if (rows <= 0 || n_groups <= 0) return hipSuccess;
-    if (group_size < 1 || group_size > kMaxGroupWaves) return hipErrorInvalidValue;
+    if (!ws_state || !decode_attention_prefix_ok(g, n_heads, group_size, shared_len)) return hipErrorInvalidValue;
     const float sl2 = kLog2e / sqrtf((float)g.head_dim);
+    // the prefix covers the shared pages inside the first context split (whole pages)
+    const int pre_keys = std::min(shared_len, g.split_keys / g.page_size * g.page_size);
+    const int pre_blocks = pre_keys >> 5;
+    const int nw = (group_size * (n_heads / g.n_kv) + 15) / 16;
     const int ms = std::max(1, (max_ctx + g.split_keys - 1) / g.split_keys);
-    dim3 grid(n_groups * g.n_kv, ms);
-    const int nw = group_size <= 4 ? 4 : (group_size <= 8 ? 8 : 16);
-#define DASH_GROUP_LAUNCH(HDV, NWV)                                                                              \
-    decode_attn_group_bf16_k<HDV, NWV><<<grid, 64 * NWV, 0, st>>>((const bf16_t*)q, pos, slot, page_table,       \
-                                                                  (const bf16_t*)pool, g, layer, n_heads, group_off, \
-                                                                  shared_len, (bf16_t*)o, ms, ws_part, sl2)
+    dim3 grid(rows * g.n_kv, ms);
     if (g.head_dim == 128) {
-        if (nw == 4) DASH_GROUP_LAUNCH(128, 4);
-        else if (nw == 8) DASH_GROUP_LAUNCH(128, 8);
-        else DASH_GROUP_LAUNCH(128, 16);
-    } else if (g.head_dim == 64) {
-        if (nw == 4) DASH_GROUP_LAUNCH(64, 4);
-        else if (nw == 8) DASH_GROUP_LAUNCH(64, 8);
-        else DASH_GROUP_LAUNCH(64, 16);
+        decode_attn_prefix_k<128><<<n_groups * g.n_kv, 64 * nw, 0, st>>>(
+            (const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool, g, layer, n_heads, group_off, pre_blocks,
+            ws_state, sl2);
+        decode_attn_bf16_k<128, true><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
+                                                            g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2, ws_state,
+                                                            pre_blocks);
     } else {
-        return hipErrorInvalidValue;
+        decode_attn_prefix_k<64><<<n_groups * g.n_kv, 64 * nw, 0, st>>>(
+            (const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool, g, layer, n_heads, group_off, pre_blocks,
+            ws_state, sl2);
+        decode_attn_bf16_k<64, true><<<grid, 64, 0, st>>>((const bf16_t*)q, pos, slot, page_table, (const bf16_t*)pool,
+                                                           g, layer, n_heads, (bf16_t*)o, ms, ws_part, sl2, ws_state,
+                                                           pre_blocks);
     }
-#undef DASH_GROUP_LAUNCH
     return hipGetLastError();
 }
 

@@ -97,14 +97,20 @@ hipError_t launch_decode_attention(int dtype, const void* q, const int32_t* pos,
 // Partial-result floats for any cache of this max_ctx (sized for the shortest split).
 size_t attention_partial_floats(int rows, int n_heads, int head_dim, int max_ctx);
 // Decode attention for batches made of groups of rows that share a prefix: rows
-// [group_off[i], group_off[i+1]) (at most group_size <= 16 of them) share their first
-// shared_len positions (the same pages, read from the group's first row).  Same
-// results as launch_decode_attention, bit for bit; bf16 only.
+// [group_off[i], group_off[i+1]) (at most group_size of them) share their first
+// shared_len positions (the same pages, read from the group's first row).  A first
+// kernel runs the shared pages (those inside the first context split) once per group
+// and kv head, leaving each row's online-softmax state in ws_state
+// (decode_attention_prefix_state_bytes), and the per-row kernel continues from it.
+// Same results as launch_decode_attention, bit for bit; bf16 only.  hipErrorInvalidValue
+// unless decode_attention_prefix_ok holds and ws_state is set.
+bool decode_attention_prefix_ok(const KVGeom& g, int n_heads, int group_size, int shared_len);
+size_t decode_attention_prefix_state_bytes(int rows, int n_heads, int head_dim);
 hipError_t launch_decode_attention_grouped(const void* q, const int32_t* pos, const int32_t* slot,
                                            const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                            int n_heads, const int32_t* group_off, int n_groups, int group_size,
                                            int shared_len, void* o, int rows, int max_ctx, float* ws_part,
-                                           hipStream_t st);
+                                           float* ws_state, hipStream_t st);
 // Second pass of decode attention: merge the splits of rows longer than one split (bf16 only).
 hipError_t launch_attention_combine(int dtype, const int32_t* pos, int rows, int n_heads, int head_dim,
                                     int max_ctx, int split_keys, const float* ws_part, void* o, hipStream_t st);

@@ -4,10 +4,14 @@
 // rewards.  Besides timing, it is the program hardware-counter runs of the rollout
 // kernels profile (a plain device copy of known size runs first, as the reference
 // for byte counters), and a usage example of include/dash.h.
+// --attn 1 then compares decode attention per row (dash_decode_step) with the
+// prefix-shared form (dash_decode_step_grouped, each prompt's G samples one group)
+// on the same batch at three context lengths: the attention kernels' time per layer
+// from the library's kernel-class timing, and the whole step's time.
 //
 //   dash_native_bench [--layers 28] [--d 1536] [--heads 12] [--kv 2] [--hd 128] [--ff 8960]
 //                     [--vocab 151936] [--prompts 128] [--group 8] [--prompt 256] [--gen 1024]
-//                     [--graph 1] [--copy-mib 1024] [--rollouts 2]
+//                     [--graph 1] [--copy-mib 1024] [--rollouts 2] [--attn 0]
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -102,7 +106,7 @@ int main(int argc, char** argv) {
     const int n_prompts = arg(argc, argv, "--prompts", 128), G = arg(argc, argv, "--group", 8);
     const int P = arg(argc, argv, "--prompt", 256), T = arg(argc, argv, "--gen", 1024);
     const int use_graph = arg(argc, argv, "--graph", 1), copy_mib = arg(argc, argv, "--copy-mib", 1024);
-    const int rollouts = arg(argc, argv, "--rollouts", 2);
+    const int rollouts = arg(argc, argv, "--rollouts", 2), attn_cmp = arg(argc, argv, "--attn", 0);
     const int N = n_prompts * G, ps = 32;
 
     hipStream_t st;
@@ -185,6 +189,58 @@ int main(int argc, char** argv) {
         CHECK_HIP(hipStreamSynchronize(st));
         const double s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
         std::printf("rollout %d: %.3f s, %.1f generated tokens/s\n", r, s, (double)N * T / s);
+    }
+
+    if (attn_cmp) {
+        // one prefill of the whole batch, then decode steps at fixed contexts (each step
+        // rewrites the K/V of its position, so the context stays the same)
+        std::vector<int32_t> slots(N);
+        for (int i = 0; i < N; ++i) slots[i] = i;
+        float* logits = (float*)dev_alloc((size_t)N * d.vocab * 4);
+        int32_t* d_slot = (int32_t*)dev_alloc((size_t)N * 4);
+        int32_t* d_pos = (int32_t*)dev_alloc((size_t)N * 4);
+        int32_t* d_tok = (int32_t*)dev_alloc((size_t)N * 4);
+        int32_t* d_off = (int32_t*)dev_alloc((size_t)(n_prompts + 1) * 4);
+        std::vector<int32_t> off(n_prompts + 1);
+        for (int i = 0; i <= n_prompts; ++i) off[i] = i * G;
+        CHECK_HIP(hipMemcpy(d_slot, slots.data(), (size_t)N * 4, hipMemcpyHostToDevice));
+        CHECK_HIP(hipMemcpy(d_off, off.data(), off.size() * 4, hipMemcpyHostToDevice));
+        fill_tokens<<<64, 256, 0, st>>>(d_tok, N, d.vocab, 99u);
+        CHECK_DASH(dash_prefill(model, kv, prompts, n_prompts, P, G, slots.data(), logits, ws, ws_bytes, st));
+        const int shared = P / ps * ps;
+        const int reps = 5;
+        for (const int c : {P + 1, (P + max_ctx) / 2, max_ctx}) {
+            CHECK_DASH(dash_kv_reserve(kv, slots.data(), N, c, st));
+            std::vector<int32_t> pos(N, c - 1);
+            CHECK_HIP(hipMemcpy(d_pos, pos.data(), (size_t)N * 4, hipMemcpyHostToDevice));
+            double attn_us[2], step_ms[2];
+            for (int v = 0; v < 2; ++v) {
+                auto step = [&]() {
+                    if (v == 0) CHECK_DASH(dash_decode_step(model, kv, d_tok, d_slot, d_pos, N, logits, ws, ws_bytes, st));
+                    else
+                        CHECK_DASH(dash_decode_step_grouped(model, kv, d_tok, d_slot, d_pos, N, d_off, n_prompts, G,
+                                                            shared, logits, ws, ws_bytes, st));
+                };
+                step();
+                step();
+                CHECK_HIP(hipStreamSynchronize(st));
+                const auto t0 = std::chrono::steady_clock::now();
+                for (int r = 0; r < reps; ++r) step();
+                CHECK_HIP(hipStreamSynchronize(st));
+                step_ms[v] = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count() / reps;
+                double ms[DASH_K_COUNT];
+                int64_t n[DASH_K_COUNT];
+                CHECK_DASH(dash_profile_read(ms, n, 1));
+                CHECK_DASH(dash_profile_enable(1u << DASH_K_ATTN));
+                for (int r = 0; r < reps; ++r) step();
+                CHECK_DASH(dash_profile_read(ms, n, 1));
+                CHECK_DASH(dash_profile_enable(0));
+                attn_us[v] = ms[DASH_K_ATTN] * 1e3 / (double)(n[DASH_K_ATTN] ? n[DASH_K_ATTN] : 1);
+            }
+            std::printf("context %d: decode attention per layer %.1f us per row, %.1f us prefix-shared; "
+                        "step %.2f ms vs %.2f ms\n", c, attn_us[0], attn_us[1], step_ms[0], step_ms[1]);
+        }
+        for (void* p : {(void*)logits, (void*)d_slot, (void*)d_pos, (void*)d_tok, (void*)d_off}) CHECK_HIP(hipFree(p));
     }
 
     dash_kv_destroy(kv);

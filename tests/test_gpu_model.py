@@ -322,6 +322,35 @@ def test_grouped_decode_bitexact_vs_per_row(shape, n_prompts, G, P, steps):
         np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("shape,n_prompts,G,P,steps", [(BF16_B, 2, 8, 600, 3), (BF16_A, 2, 4, 1100, 3)])
+def test_grouped_decode_long_prefix_bitexact(shape, n_prompts, G, P, steps):
+    """Prefix-shared decode over prompts longer than one LDS chunk of the prefix kernel
+    (18 pages at head dim 128, 32 at head dim 64, 8 / 16 pages per chunk) in a cache whose
+    slot count makes the split long enough to hold the whole prefix (and, at head dim 64,
+    contexts that still need two splits): bit-identical to the per-row kernel."""
+    w = synth.make_weights(shape, 6)
+    wl = synth.Workload("t", shape, n_prompts, G, P, steps + 1)
+    prompts = synth.make_prompts(wl, 6)
+    model = engine.Model(shape, w)
+    N = n_prompts * G
+    ps, max_ctx = 32, P + steps + 8
+    kv = engine.KVCache(model, ps, 1024, max_ctx, N * ((max_ctx + ps - 1) // ps) + 8)
+    split = L.dash_kv_split_keys(kv.handle)
+    assert split >= 512, split  # the whole shared prefix (or its first 512 keys) in split 0
+    engine.prefill(model, kv, dev_i32(prompts), G, list(range(N)))
+    shared = (P // ps) * ps
+    off = dev_i32(np.arange(0, N + 1, G))
+    rng = np.random.default_rng(1)
+    for t in range(steps):
+        L.dash_kv_reserve(kv.handle, list(range(N)), P + t + 1, engine.stream_handle())
+        toks = dev_i32(rng.integers(0, shape.vocab, N))
+        slots = dev_i32(np.arange(N))
+        pos = dev_i32(np.full(N, P + t))
+        a = engine.decode_step(model, kv, toks, slots, pos).cpu().numpy()
+        b = engine.decode_step_grouped(model, kv, toks, slots, pos, off, G, shared).cpu().numpy()
+        np.testing.assert_array_equal(a, b)
+
+
 def test_decode_halves_on_two_streams_bitexact():
     """Two halves of a batch decoded at the same time on two streams (separate workspaces,
     disjoint slots, shared prompt pages) give the full batch's logits bit for bit, at contexts
