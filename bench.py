@@ -30,7 +30,7 @@ ATTN_TRAFFIC = {
     "workload": "1.5b-b1024",
     "bytes_per_launch": 621_200_000,
     "sources": {
-        "paper_2505_17218_amd/csrc/attention.hip": "88aa7d45041ab5c45850e89d3787c6047d23e157e7d794e886967242728225db",
+        "paper_2505_17218_amd/csrc/attention.hip": "e81ece5078e4e69a20c5bd9e6a1293b628406caf0924b18cfd4523172d8523a3",
         "paper_2505_17218_amd/csrc/common.h": "16d56f2b1c378ddeb1902011b1b9beb198deb192709a5250858858f49c6d4547",
     },
 }

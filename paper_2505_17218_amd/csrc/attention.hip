@@ -278,7 +278,7 @@ __global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restric
         else
             load_kv<HD, kKvStream>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
     };
-    if (b_begin < b_end) {
+    if (!PRE || b_begin < b_end) {  // only a continued chain can be empty
         fetch(r[0], b_begin);
         for (int b = b_begin; b < b_end; b += 2) {
             fetch(r[1], min(b + 1, b_end - 1));
