@@ -690,9 +690,24 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
         // (>= 256) to pull them from HBM at full rate.
         if (epi == EPI_SWIGLU) {
             if (nsplit != 1) return hipErrorInvalidValue;
-            // Past 1024 rows 256x256 tiles (measured on the 1.5B and 3B shapes: 12% faster at
-            // 1536 rows, 15-19% at 4096-16384; 10% slower at 1024 rows on 1.5B).
-            if (M > 1024) return run_bf16<256, 256, 4, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+            if (M > 384) {
+                // Past 384 rows the tile is chosen by how its work-groups fill the 256 CUs
+                // (one 256x256 or 128x256 work-group per CU, two 128x128 ones): 256x256 where
+                // they fill one round (128-256 tiles), or leave a last round at least half
+                // full, or run four rounds or more; else 128x256 under the same test; else
+                // 128x128.  Measured with dash_gemm_bench on the 0.5B, 1.5B and 3B shapes at
+                // 512-2048 rows (weights cold, interleaved rounds): each choice the fastest
+                // tiling or within 2% of it (256x256: 1.5B 7% / 19% faster than 128x128 at
+                // 512 / 768 rows, 3B 13% at 2048; 128x128: 0.5B 20% faster than 256x256 at
+                // 2048 rows); 256x256 also measured 15-19% faster at 4096-16384 rows.
+                const long cols = (N / 2 + 127) / 128;
+                const long t256 = (M + 255) / 256 * cols, t128 = (M + 127) / 128 * cols;
+                if ((t256 >= 128 && t256 <= 256) || t256 % 256 >= 128 || t256 >= 4 * 256)
+                    return run_bf16<256, 256, 4, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+                if (t128 <= 256 || t128 % 256 >= 128)
+                    return run_bf16<128, 256, 4, 4, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+                return run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
+            }
             if (M > 256) return run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(A, W, C, M, N, K, ldc, 1, 0, st);
             // Small batches: 64 column pairs per tile read the batch rows half as often as
             // 32; worth it where that still leaves >= 128 work-groups per 64-row block
@@ -720,7 +735,10 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
             // about 160 or more work-groups.  Measured on the 0.5B, 1.5B and 3B shapes at
             // 256-2048 rows (dash_gemm_bench, weights cold): 7-36% faster than the
             // register-staged tiles (1.5B at 1024 rows: 14.8 -> 10.5 us).
-            if (M <= 512) return run_lds<64, 64, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            // 64x64 tiles while they fit one round (<= 256 work-groups): 15-17% faster than
+            // 128x64 for the 0.5B shape at 768-1024 rows
+            if ((long)((M + 63) / 64) * ((N + 63) / 64) <= 256)
+                return run_lds<64, 64, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             if (M <= 1024 || (long)(M / 128) * ((N + 127) / 128) < 160)
                 return run_lds<128, 64, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
@@ -738,8 +756,8 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
         // Larger batches: the largest tile that still gives the launch enough work-groups.
         // Measured crossovers on the 0.5B, 1.5B and 3B shapes: the split down projection
         // 64x64 three k-steps ahead up to 128 rows and two up to 384 (12-19% faster than
-        // 64x32 there), 128x256 up to 1024, 256x256 past that (12-18% faster from 1536
-        // rows); QKV / O 64x64 three k-steps ahead up to 512 rows (10-15% faster than two),
+        // 64x32 there), the direct-to-LDS 128x128 tiles up to 640, 128x256 up to 1024,
+        // 256x256 past that (12-18% faster from 1536 rows); QKV / O 64x64 three k-steps ahead up to 512 rows (10-15% faster than two),
         // 64x64 up to 1024, 128x128 up to 4096 (4-30% faster from 1536), 256x256 past that
         // (15-26% faster at 8192-16384).
         if (K >= 4096) {
@@ -747,6 +765,8 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                 return run_bf16<64, 64, 2, 2, 3, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             if (M <= 384)
                 return run_bf16<64, 64, 2, 2, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
+            if (M <= 640)  // direct-to-LDS 128x128: 23-35% faster at 512 rows on all three shapes
+                return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             if (M <= 1024)
                 return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);
             return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(A, W, C, M, N, K, ldc, nsplit, split_stride, st);

@@ -1,14 +1,19 @@
 // Micro-benchmark of the projection GEMM kernels (built as dash_gemm_bench next to
 // libdash.so): for the decoder shapes of the workloads and a range of decode batch
-// sizes, times the tiling launch_gemm / launch_gemm_qkv_rope choose against the other
-// kernels of gemm.hip, and checks that every alternative gives the same bits.  Weights
-// rotate through enough copies (>= 1 GiB in total) that every launch reads them from HBM,
-// as in a decode step where each layer's weights were evicted by the other layers.
+// sizes, times the tiling launch_gemm / launch_gemm_qkv_rope choose ("production")
+// against the other kernels of gemm.hip, and checks that every alternative gives the
+// same bits (output, QKV, gate/up and down projections).  Weights rotate through
+// enough copies (>= 1 GiB in total) that every launch reads them from HBM, as in a
+// decode step where each layer's weights were evicted by the other layers.  The
+// variants of a case are timed in interleaved rounds after a common warm-up of about
+// 20 ms, and each reports its median round: timing one variant after another instead
+// made whichever ran first up to 10% slower (clock ramp after the host-side set-up).
 //
-//   dash_gemm_bench [reps]
+//   dash_gemm_bench [reps per round]
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -35,7 +40,7 @@ namespace {
 
 struct ModelShape {
     const char* name;
-    int d, n_heads, n_kv, hd;
+    int d, n_heads, n_kv, hd, ff;
 };
 
 uint16_t to_bf16(float f) {
@@ -59,90 +64,169 @@ std::vector<uint16_t> randn_bf16(size_t n, float scale, std::mt19937& rng) {
     return v;
 }
 
-using Launch = std::function<hipError_t(const void* w)>;
+int weight_copies(int N, int K) { return (int)std::min<size_t>(16, (1ull << 30) / ((size_t)N * K * 2) + 1); }
 
-double time_us(const Launch& f, int n_w, size_t w_bytes, const void* w0, int reps, hipStream_t st) {
+// Weight copies of one projection, each read cold by the launch that uses it.
+struct Weights {
+    size_t bytes;
+    int copies;
+    Dev w;
+    Weights(int N, int K, std::mt19937& rng)
+        : bytes((size_t)N * K * 2), copies(weight_copies(N, K)), w((size_t)N * K * 2 * weight_copies(N, K)) {
+        const auto h = randn_bf16((size_t)N * K, 0.02f, rng);
+        for (int i = 0; i < copies; ++i) CK(hipMemcpy((char*)w.p + i * bytes, h.data(), bytes, hipMemcpyHostToDevice));
+    }
+    const void* copy(int i) const { return (const char*)w.p + (size_t)(i % copies) * bytes; }
+};
+
+// A variant launches into the reference outputs (ref = true) or the scratch ones.
+struct Variant {
+    std::string name;
+    std::function<hipError_t(const void* w, bool ref)> f;
+};
+
+// Runs variant 0 (production) into the reference outputs, every other variant into the
+// scratch outputs and compares (same_as_ref), then times all of them interleaved; prints
+// one line with the median microseconds per launch of each.
+void bench_case(const char* label, const std::vector<Variant>& vs, const Weights& w, int reps, hipStream_t st,
+                const std::function<void()>& clear_scratch, const std::function<bool()>& same_as_ref) {
+    std::vector<bool> same(vs.size(), true);
+    CK(vs[0].f(w.copy(0), true));
+    CK(hipStreamSynchronize(st));
+    for (size_t v = 1; v < vs.size(); ++v) {
+        clear_scratch();
+        CK(vs[v].f(w.copy(0), false));
+        CK(hipStreamSynchronize(st));
+        same[v] = same_as_ref();
+    }
+    // common warm-up: every variant over every weight copy, repeated until ~20 ms have passed
+    const auto t0 = std::chrono::steady_clock::now();
+    do {
+        for (const Variant& v : vs)
+            for (int i = 0; i < w.copies; ++i) CK(v.f(w.copy(i), false));
+        CK(hipStreamSynchronize(st));
+    } while (std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count() < 0.02);
     hipEvent_t e0, e1;
     CK(hipEventCreate(&e0));
     CK(hipEventCreate(&e1));
-    for (int i = 0; i < 3; ++i) CK(f((const char*)w0 + (i % n_w) * w_bytes));
-    CK(hipEventRecord(e0, st));
-    for (int i = 0; i < reps; ++i) CK(f((const char*)w0 + (i % n_w) * w_bytes));
-    CK(hipEventRecord(e1, st));
-    CK(hipEventSynchronize(e1));
-    float ms;
-    CK(hipEventElapsedTime(&ms, e0, e1));
+    constexpr int kRounds = 5;
+    std::vector<std::vector<double>> t(vs.size());
+    for (int r = 0; r < kRounds; ++r)
+        for (size_t v = 0; v < vs.size(); ++v) {
+            CK(hipEventRecord(e0, st));
+            for (int i = 0; i < reps; ++i) CK(vs[v].f(w.copy(i), false));
+            CK(hipEventRecord(e1, st));
+            CK(hipEventSynchronize(e1));
+            float ms;
+            CK(hipEventElapsedTime(&ms, e0, e1));
+            t[v].push_back(ms * 1e3 / reps);
+        }
     CK(hipEventDestroy(e0));
     CK(hipEventDestroy(e1));
-    return ms * 1e3 / reps;
+    printf("%s", label);
+    for (size_t v = 0; v < vs.size(); ++v) {
+        std::sort(t[v].begin(), t[v].end());
+        printf("  %s %6.1f%s", vs[v].name.c_str(), t[v][kRounds / 2], v == 0 ? "" : (same[v] ? "=" : " MISMATCH"));
+    }
+    printf("\n");
+    fflush(stdout);
+}
+
+// Compare two device buffers of n bytes.
+bool same_bytes(const Dev& x, const Dev& y) {
+    std::vector<char> a(x.n), b(y.n);
+    CK(hipMemcpy(a.data(), x.p, x.n, hipMemcpyDeviceToHost));
+    CK(hipMemcpy(b.data(), y.p, y.n, hipMemcpyDeviceToHost));
+    return a == b;
 }
 
 }  // namespace
 
 int main(int argc, char** argv) {
     const int reps = argc > 1 ? atoi(argv[1]) : 20;
-    const ModelShape shapes[] = {{"0.5b", 896, 14, 2, 64}, {"1.5b", 1536, 12, 2, 128}, {"3b", 2048, 16, 2, 128}};
+    const ModelShape shapes[] = {{"0.5b", 896, 14, 2, 64, 4864}, {"1.5b", 1536, 12, 2, 128, 8960},
+                                 {"3b", 2048, 16, 2, 128, 11008}};
     const int batches[] = {256, 512, 768, 1024, 2048};
     hipStream_t st;
     CK(hipStreamCreate(&st));
     std::mt19937 rng(7);
-    printf("kernel timings in us (weights cold); alternatives marked = give the production bits\n");
+    printf("kernel timings in us (weights cold, median of interleaved rounds); alternatives marked = give the "
+           "production bits\n");
+    char label[128];
     for (const ModelShape& sh : shapes) {
         const int d = sh.d, hq = sh.n_heads * sh.hd, qr = (sh.n_heads + 2 * sh.n_kv) * sh.hd;
         for (int M : batches) {
             // ---- output projection: C[M, d] = o[M, hq] . W_o[d, hq]^T (fp32, unsplit)
             {
                 const int N = d, K = hq;
-                const size_t w_bytes = (size_t)N * K * 2;
-                const int n_w = (int)std::min<size_t>(16, (1ull << 30) / w_bytes + 1);
-                Dev a((size_t)M * K * 2), w(w_bytes * n_w), c0((size_t)M * N * 4), c1((size_t)M * N * 4);
-                auto ha = randn_bf16((size_t)M * K, 1.f, rng), hw = randn_bf16((size_t)N * K, 0.02f, rng);
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), c0((size_t)M * N * 4), c1((size_t)M * N * 4);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
                 CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
-                for (int i = 0; i < n_w; ++i)
-                    CK(hipMemcpy((char*)w.p + i * w_bytes, hw.data(), w_bytes, hipMemcpyHostToDevice));
-                auto prod = [&](const void* wp, void* c) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, c, M, N, K, N, 1, 0, st); };
-                CK(prod(w.p, c0.p));
-                CK(hipStreamSynchronize(st));
-                std::vector<char> r0((size_t)M * N * 4), r1(r0.size());
-                CK(hipMemcpy(r0.data(), c0.p, r0.size(), hipMemcpyDeviceToHost));
-                const double tp = time_us([&](const void* wp) { return prod(wp, c1.p); }, n_w, w_bytes, w.p, reps, st);
-                printf("%-5s o    M=%4d N=%4d K=%4d  production %7.1f", sh.name, M, N, K, tp);
-                struct Alt {
-                    const char* name;
-                    std::function<hipError_t(const void*, void*)> f;
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"lds128x64", [&](const void* wp, bool r) { return run_lds<128, 64, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"lds64x64", [&](const void* wp, bool r) { return run_lds<64, 64, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"lds64x128", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"lds128x128", [&](const void* wp, bool r) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
                 };
-                const Alt alts[] = {
-                    {"lds128x64", [&](const void* wp, void* c) { return run_lds<128, 64, 2, 2, 4, EPI_STORE_F32>(a.p, wp, c, M, N, K, N, 1, 0, st); }},
-                    {"lds64x64", [&](const void* wp, void* c) { return run_lds<64, 64, 2, 2, 4, EPI_STORE_F32>(a.p, wp, c, M, N, K, N, 1, 0, st); }},
-                    {"lds64x128", [&](const void* wp, void* c) { return run_lds<64, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, c, M, N, K, N, 1, 0, st); }},
-                    {"lds128x128", [&](const void* wp, void* c) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, c, M, N, K, N, 1, 0, st); }},
+                snprintf(label, sizeof label, "%-5s o    M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            }
+            // ---- gate/up projection with the SwiGLU epilogue: h[M, ff] (bf16), unsplit
+            if (M >= 512) {
+                const int ff = sh.ff, N = 2 * ff, K = d;
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), c0((size_t)M * ff * 2), c1((size_t)M * ff * 2);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_SWIGLU, a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"128x128w8", [&](const void* wp, bool r) { return run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"128x128w4", [&](const void* wp, bool r) { return run_bf16<128, 128, 2, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
                 };
-                for (const Alt& alt : alts) {
-                    CK(hipMemset(c1.p, 0xFF, r1.size()));
-                    CK(alt.f(w.p, c1.p));
-                    CK(hipStreamSynchronize(st));
-                    CK(hipMemcpy(r1.data(), c1.p, r1.size(), hipMemcpyDeviceToHost));
-                    const bool same = memcmp(r0.data(), r1.data(), r0.size()) == 0;
-                    const double t = time_us([&](const void* wp) { return alt.f(wp, c1.p); }, n_w, w_bytes, w.p, reps, st);
-                    printf("  %s %6.1f%s", alt.name, t, same ? "=" : " MISMATCH");
-                }
-                printf("\n");
-                fflush(stdout);
+                snprintf(label, sizeof label, "%-5s gu   M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            }
+            // ---- down projection: fp32 split-K partials [splits][M, d]
+            if (M >= 512) {
+                const int N = d, K = sh.ff;
+                const int ns = gemm_pick_splits(1, EPI_STORE_F32, N, K);
+                Weights w(N, K, rng);
+                const size_t cn = (size_t)ns * M * N, ss = (size_t)M * N;
+                Dev a((size_t)M * K * 2), c0(cn * 4), c1(cn * 4);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"lds128x128", [&](const void* wp, bool r) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                };
+                snprintf(label, sizeof label, "%-5s down M=%4d N=%5d K=%5d s%d  ", sh.name, M, N, K, ns);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
             }
             // ---- QKV projection with bias, RoPE and the KV append (fused epilogue)
             if (gemm_qkv_fusable(1, sh.n_heads, sh.n_kv, sh.hd)) {
                 const int N = qr, K = d, hd = sh.hd, ps = 32;
-                const size_t w_bytes = (size_t)N * K * 2;
-                const int n_w = (int)std::min<size_t>(16, (1ull << 30) / w_bytes + 1);
-                Dev a((size_t)M * K * 2), w(w_bytes * n_w), bias((size_t)N * 2), cs((size_t)M * hd * 4);
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), bias((size_t)N * 2), cs((size_t)M * hd * 4);
                 Dev pos((size_t)M * 4), slot((size_t)M * 4), table((size_t)M * 4), status(256);
                 const size_t pool_elems = (size_t)M * sh.n_kv * 2 * ps * hd;  // one page per row, one layer
                 Dev pool0(pool_elems * 2), pool1(pool_elems * 2), q0((size_t)M * hq * 2), q1((size_t)M * hq * 2);
-                auto ha = randn_bf16((size_t)M * K, 1.f, rng), hw = randn_bf16((size_t)N * K, 0.02f, rng);
-                auto hb = randn_bf16(N, 0.02f, rng);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                const auto hb = randn_bf16(N, 0.02f, rng);
                 CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
-                for (int i = 0; i < n_w; ++i)
-                    CK(hipMemcpy((char*)w.p + i * w_bytes, hw.data(), w_bytes, hipMemcpyHostToDevice));
                 CK(hipMemcpy(bias.p, hb.data(), hb.size() * 2, hipMemcpyHostToDevice));
                 std::vector<int32_t> hp(M), hs(M), ht(M);
                 std::vector<float> hcs((size_t)M * hd);
@@ -161,52 +245,34 @@ int main(int argc, char** argv) {
                 CK(hipMemcpy(table.p, ht.data(), M * 4, hipMemcpyHostToDevice));
                 CK(hipMemcpy(cs.p, hcs.data(), hcs.size() * 4, hipMemcpyHostToDevice));
                 CK(hipMemset(status.p, 0, 4));
-                KVGeom g{1, M, sh.n_kv, hd, ps, 1, M, 2048, 0};
-                auto args = [&](void* pool, void* q) {
-                    return QkvRopeArgs{(const bf16_t*)bias.p, (const float*)cs.p, (const int32_t*)pos.p,
-                                       (const int32_t*)slot.p, (const int32_t*)table.p, (bf16_t*)pool, g, 0,
-                                       (bf16_t*)q, sh.n_heads, (uint32_t*)status.p};
-                };
                 CK(hipMemset(pool0.p, 0, pool0.n));
                 CK(hipMemset(pool1.p, 0, pool1.n));
-                // the production path (fused above its size threshold, else the unfused GEMM + RoPE kernel)
-                auto prod = [&](const void* wp, void* pool, void* q) -> hipError_t {
-                    const QkvRopeArgs qa = args(pool, q);
-                    if (gemm_qkv_fuse_pays(M, N)) return launch_gemm_qkv_rope(a.p, wp, M, N, K, qa, st);
-                    return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, qa);
+                const KVGeom g{1, M, sh.n_kv, hd, ps, 1, M, 2048, 0};
+                auto args = [&](bool ref) {
+                    return QkvRopeArgs{(const bf16_t*)bias.p, (const float*)cs.p, (const int32_t*)pos.p,
+                                       (const int32_t*)slot.p, (const int32_t*)table.p,
+                                       (bf16_t*)(ref ? pool0.p : pool1.p), g, 0, (bf16_t*)(ref ? q0.p : q1.p),
+                                       sh.n_heads, (uint32_t*)status.p};
                 };
-                CK(prod(w.p, pool0.p, q0.p));
-                CK(hipStreamSynchronize(st));
-                std::vector<char> rq0(q0.n), rp0(pool0.n), rq1(q0.n), rp1(pool0.n);
-                CK(hipMemcpy(rq0.data(), q0.p, q0.n, hipMemcpyDeviceToHost));
-                CK(hipMemcpy(rp0.data(), pool0.p, pool0.n, hipMemcpyDeviceToHost));
-                const double tp = time_us([&](const void* wp) { return prod(wp, pool1.p, q1.p); }, n_w, w_bytes, w.p,
-                                          reps, st);
-                printf("%-5s qkv  M=%4d N=%4d K=%4d  fused     %7.1f", sh.name, M, N, K, tp);
-                struct Alt {
-                    const char* name;
-                    std::function<hipError_t(const void*, void*, void*)> f;
+                const std::vector<Variant> vs = {
+                    // the production path: fused above its size threshold, else the unfused GEMM + RoPE kernel
+                    {"production", [&](const void* wp, bool r) -> hipError_t {
+                         if (gemm_qkv_fuse_pays(M, N)) return launch_gemm_qkv_rope(a.p, wp, M, N, K, args(r), st);
+                         return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r));
+                     }},
+                    {"lds64x128", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"lds64x128s3", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
                 };
-                const Alt alts[] = {
-                    {"lds64x128", [&](const void* wp, void* pool, void* q) { return run_lds<64, 128, 2, 2, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(pool, q)); }},
-                    {"lds64x128s3", [&](const void* wp, void* pool, void* q) { return run_lds<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(pool, q)); }},
-                };
-                for (const Alt& alt : alts) {
-                    CK(hipMemset(pool1.p, 0, pool1.n));
-                    CK(hipMemset(q1.p, 0xFF, q1.n));
-                    CK(alt.f(w.p, pool1.p, q1.p));
-                    CK(hipStreamSynchronize(st));
-                    CK(hipMemcpy(rq1.data(), q1.p, q1.n, hipMemcpyDeviceToHost));
-                    CK(hipMemcpy(rp1.data(), pool1.p, pool1.n, hipMemcpyDeviceToHost));
-                    const bool same = rq0 == rq1 && rp0 == rp1;
-                    const double t = time_us([&](const void* wp) { return alt.f(wp, pool1.p, q1.p); }, n_w, w_bytes,
-                                             w.p, reps, st);
-                    printf("  %s %6.1f%s", alt.name, t, same ? "=" : " MISMATCH");
-                }
+                snprintf(label, sizeof label, "%-5s qkv  M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
+                bench_case(label, vs, w, reps, st,
+                           [&] {
+                               CK(hipMemset(pool1.p, 0, pool1.n));
+                               CK(hipMemset(q1.p, 0xFF, q1.n));
+                           },
+                           [&] { return same_bytes(q0, q1) && same_bytes(pool0, pool1); });
                 uint32_t hst = 0;
                 CK(hipMemcpy(&hst, status.p, 4, hipMemcpyDeviceToHost));
-                printf("%s\n", hst ? "  (status set!)" : "");
-                fflush(stdout);
+                if (hst) printf("  (status set!)\n");
             }
         }
     }

@@ -172,13 +172,13 @@ def test_bf16_gemm_tile_regimes(n_prompts):
         np.testing.assert_array_equal(small.logits[0], run.logits[0][:40])
 
 
-# d_ff = 2240 (35 SwiGLU tile columns of 64): a 1024-row decode batch runs gate/up on
-# 128x128 tiles with a partial last round, a 40-row batch on 64x64 tiles
+# d_ff = 2240 (18 columns of 128-wide SwiGLU tile pairs): a 1024-row decode batch runs
+# gate/up on 128x256 tiles (144, under one round), a 40-row batch on 64x64 tiles
 BF16_E = synth.Shape("bf16-ff2240", 1, 256, 4, 2, 64, 2240, 500, 1e6, synth.DT_BF16)
 
 
 def test_bf16_swiglu_tile_regimes_bitexact():
-    """1024 decode rows (128x128 SwiGLU tiles) give every row the same logits, bit for bit,
+    """1024 decode rows (128x256 SwiGLU tiles) give every row the same logits, bit for bit,
     as a 40-row batch (64x64 tiles), and match the oracle."""
     shape = BF16_E
     w = synth.make_weights(shape, 9)
@@ -194,12 +194,38 @@ def test_bf16_swiglu_tile_regimes_bitexact():
         assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
 
 
+# d_ff = 8320 (65 columns of 128-wide SwiGLU tile pairs): at 1024 rows neither one round of
+# 256x256 tiles (260 > 256) nor 128x256 tiles with a well-filled last round (520 = 2 x 256 + 8)
+# fit, so gate/up runs on 128x128 tiles; 40 rows on 64x64 tiles
+BF16_I = synth.Shape("bf16-ff8320", 1, 256, 4, 2, 64, 8320, 500, 1e6, synth.DT_BF16)
+
+
+def test_bf16_swiglu_tile_rounds_bitexact():
+    """The 1024-row gate/up tiling chosen by how the tiles fill the GPU (128x128 here) gives
+    the rows it shares with a 40-row batch the same logits, bit for bit, and matches the
+    oracle."""
+    shape = BF16_I
+    w = synth.make_weights(shape, 12)
+    wl = synth.Workload("t", shape, 256, 4, 10, 2)
+    prompts = synth.make_prompts(wl, 12)
+    model = engine.Model(shape, w)
+    big = run_stepwise(model, make_kv(model, 32, 1024, 12), prompts, 4, 2, 1.0, 5)
+    small = run_stepwise(model, make_kv(model, 32, 40, 12), prompts[:10], 4, 2, 1.0, 5)
+    np.testing.assert_array_equal(small.logits[1], big.logits[1][:40])  # the decode step (M = 1024 vs 40)
+    sd = shape_dict(shape)
+    for n in (0, 517, 1023):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], big.tokens[n])
+        assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
+
+
 # d_ff = 8192 (128 SwiGLU tiles of 64 column pairs): gate/up runs on 64x128 tiles with three
 # k-steps in flight up to 64 rows, on 64x64 tiles at 65-128 rows, on 64x128 tiles with two
-# k-steps in flight at 129-256 rows, on 128x128 tiles up to 1024 rows and on 256x256 past
-# that; the down projection (K = 8192, split) on 64x32 tiles four k-steps ahead, 64x64
-# tiles three or two k-steps ahead, 128x256 or 256x256; the output projection on 64x32
-# tiles, 64x64 tiles three or two k-steps ahead, 128x128 or 256x256 tiles
+# k-steps in flight at 129-256 rows, on 128x128 tiles at 300 rows, on 256x256 tiles at 480
+# and 1024 rows (one round of 128 / 256 of them) and on 128x128 tiles again at 2048 rows
+# (512 = two exact rounds of 256x256, 1024 = four of 128x256); the down projection
+# (K = 8192, split) on 64x32 tiles four k-steps ahead, 64x64 tiles three or two k-steps
+# ahead, direct-to-LDS 128x128 tiles (480 rows), 128x256 or 256x256; the output projection
+# on 64x32 tiles, 64x64 tiles three or two k-steps ahead, direct-to-LDS or 256x256 tiles
 BF16_G = synth.Shape("bf16-ff8192", 1, 256, 4, 2, 64, 8192, 500, 1e6, synth.DT_BF16)
 
 
