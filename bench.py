@@ -30,7 +30,7 @@ ATTN_TRAFFIC = {
     "workload": "1.5b-b1024",
     "bytes_per_launch": 621_200_000,
     "sources": {
-        "paper_2505_17218_amd/csrc/attention.hip": "e81ece5078e4e69a20c5bd9e6a1293b628406caf0924b18cfd4523172d8523a3",
+        "paper_2505_17218_amd/csrc/attention.hip": "8797ed6308e9473008fe38b1ea497e707d0e0c0aa07e14fd7a6a31dd5a3e5a25",
         "paper_2505_17218_amd/csrc/common.h": "16d56f2b1c378ddeb1902011b1b9beb198deb192709a5250858858f49c6d4547",
     },
 }

@@ -216,8 +216,12 @@ DASH_DEV void attn_state_load(AttnState<HD>& st, const float* sp, int grp) {
 
 // ---- decode ----------------------------------------------------------------
 
+// Head dim 64 asks the compiler for four waves per SIMD (122 registers instead of 150:
+// 9-10% less attention time at 257-768 keys for the 0.5B shape); head dim 128 keeps its
+// two (the same target there gave it 211 registers and was 2% slower at 1280 keys).
 template <int HD, bool PRE = false>
-__global__ void __launch_bounds__(64) decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(HD == 64 ? 4 : 1)))
+decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos,
                                                          const int32_t* __restrict__ slot,
                                                          const int32_t* __restrict__ page_table,
                                                          const bf16_t* __restrict__ pool, KVGeom g, int layer,
@@ -592,9 +596,10 @@ __global__ void __launch_bounds__(64) attn_generic_k(const T* __restrict__ q, co
 
 int attention_split_keys(int max_seqs, int n_kv, int max_ctx, int head_dim) {
     const auto waves = [&](long s) { return (long)max_seqs * n_kv * ((max_ctx + s - 1) / s); };
-    // as many waves as fit the GPU at once: the hd-64 kernel's registers allow three per
-    // SIMD, the hd-128 kernel's two (at 512 sequences of the 0.5B shape the longer target
-    // halves the split length: 18% less attention time)
+    // about as many waves as fit the GPU at once: the hd-128 kernel's registers allow two
+    // per SIMD; for hd 64 (four per SIMD) three per SIMD measured best (at 512 sequences of
+    // the 0.5B shape: split 512, 18% less attention time than split 1024, and the whole
+    // rollout 2% faster than split 256)
     const long target = head_dim == 64 ? 3L * kAttnTargetWaves / 2 : kAttnTargetWaves;
     int s = kAttnMinSplitKeys;
     while (s < max_ctx && s < (1 << 20) && waves(2L * s) >= target) s *= 2;
