@@ -2,7 +2,7 @@
 // libdash.so): for the decoder shapes of the workloads and a range of decode batch
 // sizes, times the tiling launch_gemm / launch_gemm_qkv_rope choose ("production")
 // against the other kernels of gemm.hip, and checks that every alternative gives the
-// same bits (output, QKV, gate/up and down projections).  Weights rotate through
+// same bits (output, QKV, gate/up, down projections and the 1.5B LM head).  Weights rotate through
 // enough copies (>= 1 GiB in total) that every launch reads them from HBM, as in a
 // decode step where each layer's weights were evicted by the other layers.  The
 // variants of a case are timed in interleaved rounds after a common warm-up of about
@@ -214,6 +214,25 @@ int main(int argc, char** argv) {
                 };
                 snprintf(label, sizeof label, "%-5s down M=%4d N=%5d K=%5d s%d  ", sh.name, M, N, K, ns);
                 bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            }
+            // ---- LM head (tied embedding, fp32 logits over the whole vocabulary), on the 1.5B shape
+            if (M >= 512 && sh.d == 1536) {
+                const int N = 151936, K = d;
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), c0((size_t)M * N * 4), c1((size_t)M * N * 4);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"lds128x128", [&](const void* wp, bool r) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                };
+                snprintf(label, sizeof label, "%-5s lm   M=%4d N=%6d K=%4d    ", sh.name, M, N, K);
+                bench_case(label, vs, w, std::max(2, reps / 8), st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
                            [&] { return same_bytes(c0, c1); });
             }
             // ---- QKV projection with bias, RoPE and the KV append (fused epilogue)
