@@ -281,6 +281,9 @@ int main(int argc, char** argv) {
                      }},
                     {"lds64x128", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
                     {"lds64x128s3", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128w4pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
                 };
                 snprintf(label, sizeof label, "%-5s qkv  M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
                 bench_case(label, vs, w, reps, st,
