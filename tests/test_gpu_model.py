@@ -377,6 +377,25 @@ def test_grouped_decode_long_prefix_bitexact(shape, n_prompts, G, P, steps):
         np.testing.assert_array_equal(a, b)
 
 
+def test_grouped_decode_argument_errors():
+    """dash_decode_step_grouped rejects, before any launch, groups above 8 rows, a shared
+    length that is not a multiple of the page size or exceeds max_ctx, and bad group counts."""
+    shape = BF16_B
+    w = synth.make_weights(shape, 5)
+    model = engine.Model(shape, w)
+    kv = make_kv(model, 32, 8, 64)
+    toks, slots, pos = dev_i32(np.zeros(8)), dev_i32(np.arange(8)), dev_i32(np.full(8, 40))
+    off = dev_i32([0, 8])
+    for group_size, shared, want in ((9, 32, L.DASH_ENOTSUP), (8, 20, L.DASH_EINVAL), (8, 96, L.DASH_EINVAL),
+                                     (8, -32, L.DASH_EINVAL)):
+        with pytest.raises(L.DashError) as e:
+            engine.decode_step_grouped(model, kv, toks, slots, pos, off, group_size, shared)
+        assert e.value.status == want, (group_size, shared)
+    with pytest.raises(L.DashError) as e:  # more groups than rows
+        engine.decode_step_grouped(model, kv, toks[:1], slots[:1], pos[:1], dev_i32([0, 1, 1]), 8, 32)
+    assert e.value.status == L.DASH_EINVAL
+
+
 def test_decode_halves_on_two_streams_bitexact():
     """Two halves of a batch decoded at the same time on two streams (separate workspaces,
     disjoint slots, shared prompt pages) give the full batch's logits bit for bit, at contexts
