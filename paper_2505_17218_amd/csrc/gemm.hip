@@ -82,6 +82,14 @@ DASH_DEV void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14));
 }
 
+// s_waitcnt vmcnt(n) lgkmcnt(0): the vector-memory wait, and every LDS read this wave
+// has issued has returned its data (n < 64)
+template <int n>
+DASH_DEV void wait_vmcnt_lds_reads() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0070 | (n & 15) | ((n >> 4) << 14));
+}
+
 // ---- epilogues shared by the GEMM kernels ------------------------------------
 // acc[i * TN + j][r] of a wave holds row (r / 4) * 8 + (lane / 32) * 4 + r % 4 and column
 // lane % 32 of its 32 x 32 block (i, j).
@@ -401,9 +409,14 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
 }
 
 // The same product with the direct-to-LDS operand path: S LDS stages, one barrier per
-// k-step.  At step k a wave waits until its own part of step k has landed, the barrier
-// then guarantees every wave's part (and that every wave is done with step k - 1), the
-// stage of step k - 1 is refilled with step k + S - 1, and step k is multiplied.  Each
+// k-step.  At step k a wave waits until its own part of step k has landed and its own
+// reads of step k - 1's stage have returned; the barrier then guarantees every wave's
+// part and that no wave still reads step k - 1's stage, which is refilled with step
+// k + S - 1, and step k is multiplied.  The wait for the reads matters: a copy into LDS
+// is written whenever its data comes back from memory, in no order with LDS reads other
+// waves have issued but not completed, so without it a slow read could see the next
+// step's data.  (That happened with two decode steps running at once on two streams:
+// 32-row blocks of some rows' outputs changed from run to run.)  Each
 // stage is its own LDS variable, so the compiler lets the loads of the other stages stay
 // in flight while a stage is read.  Same fragments, same MFMA order as gemm_bf16_k:
 // identical results.  Measured on the 1.5B decode shapes at 1024 rows (weights cold):
@@ -509,7 +522,7 @@ gemm_lds_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __r
 #define DASH_LDS_STEP(ST, KK)                                                                               \
     do {                                                                                                   \
         const int k_ = (KK);                                                                               \
-        wait_vmcnt<(S - 2) * DPS>();                                                                       \
+        wait_vmcnt_lds_reads<(S - 2) * DPS>();                                                             \
         __builtin_amdgcn_s_barrier();                                                                      \
         lds_dma_stage<AI, BI>(stage(((ST) + S - 1) % S), A, a_bytes, W, w_bytes, a_off, b_off,              \
                               step_bytes(k_ + S - 1), wave, WPOL);                                         \

@@ -127,6 +127,47 @@ def test_fullsize_decode_step_logits_elementwise(rollout_1p5b):
         assert np.sqrt((err ** 2).mean()) <= tol_rms, n
 
 
+def test_fullsize_concurrent_half_batches_bitexact(rollout_1p5b):
+    """Two 512-row halves of the 1024-row decode step running at the same time on two
+    streams (own workspaces and logits, one cache) give the full step's logits bit for bit,
+    round after round.  At 512 rows the output and down projections run on the
+    direct-to-LDS GEMM, whose stage refill must wait until no wave still reads the stage;
+    without that wait, contention between the two halves changed 32-row blocks of the
+    logits in most rounds."""
+    r = rollout_1p5b
+    wl = r["wl"]
+    model, kv = r["model"], r["kv"]
+    N, P, G, V = wl.n_seqs, wl.prompt_len, wl.group, wl.shape.vocab
+    H = N // 2
+    slots = list(range(N))
+    engine.prefill(model, kv, torch.from_numpy(r["prompts"]).cuda(), G, slots, ws=model.workspace(8 * P, 0))
+    L.dash_kv_reserve(kv.handle, slots, P + 1, engine.stream_handle())
+    toks, d_slots, pos = dev_i32(r["toks"][:, 0]), dev_i32(np.arange(N)), dev_i32(np.full(N, P))
+    full = engine.decode_step(model, kv, toks, d_slots, pos).cpu().numpy()
+    wsa, wsb = model.workspace(H, kv.max_ctx), model.workspace(N - H, kv.max_ctx)
+    lg = torch.empty(N, V, dtype=torch.float32, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    cur = torch.cuda.current_stream()
+    try:
+        for rnd in range(4):
+            lg.fill_(float("nan"))
+            for st in (s1, s2):
+                st.wait_stream(cur)
+            # both halves rewrite this step's K/V with the values the full step wrote
+            with torch.cuda.stream(s1):
+                engine.decode_step(model, kv, toks[:H], d_slots[:H], pos[:H], wsa, lg[:H])
+            with torch.cuda.stream(s2):
+                engine.decode_step(model, kv, toks[H:], d_slots[H:], pos[H:], wsb, lg[H:])
+            cur.wait_stream(s1)
+            cur.wait_stream(s2)
+            got = lg.cpu().numpy()
+            bad = np.nonzero((got != full).any(axis=1))[0]
+            assert bad.size == 0, f"round {rnd}: {bad.size} rows differ, first {bad[:8].tolist()}"
+    finally:
+        torch.cuda.synchronize()
+        L.dash_kv_release(kv.handle, slots)
+
+
 @pytest.mark.parametrize("base,rows", [("1.5b-b1024", 1024), ("3b-b2048", 2048)])
 def test_real_width_shallow_logits_strict(base, rows):
     """The real layer widths and vocabulary (1.5B: d 1536, d_ff 8960; 3B: d 2048, d_ff 11008;
