@@ -126,7 +126,7 @@ int32_t dash_weight_count(const dash_model_desc* desc);
  *   +5 w_gate_up [2 d_ff, d_model]                             rows: gate, then up
  *   +6 w_down    [d_model, d_ff]
  * Every pointer must be 16-byte aligned.  Shapes the kernels cover
- * (d_model <= 4096 always):
+ * (d_model <= 4096 and vocab <= 2^28 always):
  *   DASH_BF16: head_dim in {64, 128}, d_model % 64 == 0, d_ff % 64 == 0,
  *              n_heads / n_kv_heads <= 16;
  *   DASH_F32:  head_dim <= 128, d_model, d_ff multiples of 4.
@@ -308,7 +308,7 @@ int dash_decode_step_grouped(dash_model* model, dash_kv* kv, const int32_t* d_to
  * log softmax(l / T)_v = l_v / T - that second value for any v (both NaN for a
  * row without a finite logit); d_status (nullable, device uint32): bits OR-ed
  * in, DASH_ST_NO_FINITE_LOGIT when a row has no finite logit.  DASH_EINVAL if
- * temperature <= 0 or not finite, vocab < 1, or ld < vocab.
+ * temperature <= 0 or not finite, vocab < 1 or > 2^28, or ld < vocab.
  */
 int dash_sample(const float* d_logits, int64_t ld, int32_t n_rows, int32_t vocab, const int32_t* d_row_of,
                 const int32_t* d_seq_uid, const int32_t* d_step, float temperature, uint64_t seed,

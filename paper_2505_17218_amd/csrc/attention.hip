@@ -31,7 +31,6 @@ namespace dash {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBufferDword3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family): out-of-range reads give 0
 // Cache policies of the K/V block loads.  Decode streams (non-temporal) the blocks
 // that only one row reads: measured on gfx950 with the last-level cache cold, the
 // plain policy streams the cache at ~4.4 TB/s and the non-temporal one at ~6.0 TB/s.

@@ -14,6 +14,10 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+// Fourth dword of a raw buffer resource on gfx9-family GPUs (stride 0, 32-bit data
+// format): loads past num_records return zeros without touching memory.
+constexpr int kBufferDword3 = 0x00020000;
+
 DASH_DEV float bf2f(bf16_t u) { return __uint_as_float(static_cast<uint32_t>(u) << 16); }
 
 // float -> bfloat16, round to nearest even (NaN stays NaN).

@@ -29,9 +29,6 @@ namespace {
 
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
-// Fourth dword of a raw buffer resource on gfx9-family GPUs (stride 0, 32-bit data
-// format): loads past num_records return zeros.
-constexpr int kBufferDword3 = 0x00020000;
 
 DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 

@@ -359,6 +359,7 @@ int dash_model_create(const dash_model_desc* d, const void* const* w, int32_t n_
     if (d->n_layers < 1 || d->d_model < 1 || d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 2 ||
         d->d_ff < 1 || d->vocab < 1)
         return fail(DASH_EINVAL, "dash_model_create: non-positive dimension");
+    if (d->vocab > (1 << 28)) return fail(DASH_EINVAL, "vocab %d exceeds 2^28", d->vocab);
     if (d->n_heads % d->n_kv_heads) return fail(DASH_EINVAL, "n_heads %% n_kv_heads != 0");
     if (d->head_dim % 2) return fail(DASH_EINVAL, "head_dim must be even (RoPE pairs)");
     if (d->dtype != DASH_F32 && d->dtype != DASH_BF16) return fail(DASH_EINVAL, "dtype must be DASH_F32 or DASH_BF16");
@@ -913,7 +914,7 @@ int dash_sample(const float* logits, int64_t ld, int32_t rows, int32_t vocab, co
                 const int32_t* uid, const int32_t* step, float temperature, uint64_t seed, int32_t* tok_out,
                 float* lp_out, float* row_max_lse, uint32_t* d_status, void* stream) {
     if (!logits || !uid || !step || !tok_out) return fail(DASH_EINVAL, "dash_sample: NULL argument");
-    if (rows < 0 || vocab < 1 || ld < vocab) return fail(DASH_EINVAL, "dash_sample: bad sizes");
+    if (rows < 0 || vocab < 1 || vocab > (1 << 28) || ld < vocab) return fail(DASH_EINVAL, "dash_sample: bad sizes");
     if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DASH_EINVAL, "temperature must be > 0 and finite");
     if (rows == 0) return DASH_OK;
     ProfScope ps(DASH_K_SAMPLE, (hipStream_t)stream);

@@ -42,6 +42,18 @@ constexpr float kScreenTol = 1.6e-5f;
 
 DASH_DEV bool better(float s, int i, float bs, int bi) { return s > bs || (s == bs && i < bi); }
 
+// One entry x into an online (max mx, sum z of e^(v - mx)): a new maximum rescales the
+// sum (z e^(mx - x) + 1), any other entry adds e^(x - mx).  Both cases are one
+// exponential of -|x - mx| (x - mx and mx - x are exact negations), chosen without a
+// branch; the sampler and the log-prob gather share it, so they sum in the same way.
+DASH_DEV void lse_push(float& mx, float& z, float x) {
+    const float d = x - mx;  // +inf while mx is -inf
+    const float e = __expf(-fabsf(d));
+    const bool up = d > 0.f;
+    z = up ? z * e + 1.0f : z + e;
+    mx = up ? x : mx;
+}
+
 // Non-temporal (streaming) vector load, for logits read once.
 DASH_DEV float4 load_stream4(const float* p) {
     const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
@@ -69,6 +81,44 @@ DASH_DEV float wave_max_f(float v) {
     return v;
 }
 
+// Raw words of entries 4g .. 4g+3 of a row through a buffer resource over the row:
+// the same load instructions for every lane and every g, no branch (entries past the
+// resource read as zeros without a memory access), so the compiler's wait before a
+// group is used covers only the loads issued before it, not the ones still ahead.
+// VEC4 rows (16-byte aligned, vocab % 4 == 0) are read in 16-byte groups, other rows
+// word by word.  The caller masks entries >= vocab (vocab_mask).
+DASH_DEV __amdgpu_buffer_rsrc_t row_rsrc(const float* row, int vocab) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), 0, vocab * 4, kBufferDword3);
+}
+template <bool VEC4>
+DASH_DEV void fetch_raw4(__amdgpu_buffer_rsrc_t rs, int g, float (&l)[4]) {
+    const uint32_t off = (uint32_t)g * 16u;
+    if constexpr (VEC4) {
+        const f32x4_t v = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+        l[0] = v[0]; l[1] = v[1]; l[2] = v[2]; l[3] = v[3];
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            l[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4u * j, 0, 0));
+    }
+}
+// A register copy the compiler must keep.  The loop below copies a group out of its
+// load registers before the next load into them; with a plain copy the compiler kept
+// the group in the load registers, sent the next load elsewhere and moved the sets
+// back at the end of the iteration, which needs every load to have landed.
+DASH_DEV float copy_out(float v) {
+    float r;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(r) : "v"(v));
+    return r;
+}
+
+// Entries at or past vocab become NaN (skipped like any non-finite logit).
+DASH_DEV void vocab_mask(float (&l)[4], int g, int vocab) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (4 * g + j >= vocab) l[j] = NAN;
+}
+
 // Entries 4g .. 4g+3 of a row (NaN past the vocabulary or for g >= n4): one 16-byte
 // load when the row allows it.
 DASH_DEV void fetch4(const float* row, int g, int n4, int vocab, int vec4, float (&l)[4]) {
@@ -82,21 +132,22 @@ DASH_DEV void fetch4(const float* row, int g, int n4, int vocab, int vec4, float
 }
 
 // UNIT_T: temperature 1, no division (a runtime select would still evaluate the
-// exact division for every entry).  The next iteration's entries are loaded before
-// the current ones are scored, so their latency overlaps the arithmetic.
+// exact division for every entry).  The entries of the next two iterations are in
+// flight while the current ones are scored, so their latency overlaps the arithmetic
+// (with the earlier per-lane branches around the loads the compiler waited for every
+// outstanding load before scoring, and only the noise generation hid the latency).
 // TRAJ: the launch writes the trajectory outputs (traj, traj_lp) instead of the per-row
 // ones (lp_out, row_ml).  The output pointers stay in scalar registers through the
 // vocabulary loop: with all six of them live the kernel took 82 scalar registers and
 // ran 30% slower (250 vs 190 us at 1024 x 151,936 on gfx950) than with 70-76, the
 // same instructions otherwise.  Scalar registers are allocated in blocks of 16, so 82
 // occupies 96 of them per wave where 76 occupies 80.
-template <bool UNIT_T, bool TRAJ>
+template <bool UNIT_T, bool TRAJ, bool VEC4>
 __global__ void __launch_bounds__(kThreads)
 sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t* __restrict__ row_of,
          const int32_t* __restrict__ uid, const int32_t* __restrict__ step, float temperature, uint32_t k0,
          uint32_t k1, int32_t* __restrict__ tok_out, float* __restrict__ lp_out, float* __restrict__ row_ml,
-         uint32_t* __restrict__ status, int32_t* __restrict__ traj, float* __restrict__ traj_lp, int traj_ld,
-         int vec4) {
+         uint32_t* __restrict__ status, int32_t* __restrict__ traj, float* __restrict__ traj_lp, int traj_ld) {
     __shared__ float red_s[kThreads / 64];
     __shared__ int red_i[kThreads / 64];
     __shared__ float red_m[kThreads / 64];
@@ -111,17 +162,21 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     float mx = -INFINITY, z = 0.f;
     float floor_w = -INFINITY;  // wave-shared lower bound on the best exact score seen
     const int n4 = (vocab + 3) >> 2;
-    // every lane of the wave runs the same number of iterations (the shared bound needs all lanes)
-    const int lane0 = threadIdx.x & ~63;
-    float nxt[4];
-    fetch4(row, lane0 + (threadIdx.x & 63), n4, vocab, vec4, nxt);
-    for (int g0 = lane0; g0 < n4; g0 += kThreads) {
-        const int g = g0 + (threadIdx.x & 63);
-        float l[4] = {nxt[0], nxt[1], nxt[2], nxt[3]};
-        fetch4(row, g + kThreads, n4, vocab, vec4, nxt);
+    // every lane of the wave runs the same number of iterations (the shared bound needs all
+    // lanes); the loop counter lives in a scalar register, so its branches are uniform
+    const int lane0 = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63);
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, vocab);
+    // Scores one group of four entries of this lane (g = its group) and refreshes the
+    // wave's shared bound.
+    auto score4 = [&](float (&l)[4], int g) {
+        vocab_mask(l, g, vocab);
         float floor_t = floor_w;
         if (g < n4) {
-            const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, k0, k1);
+            // the round keys are derived here rather than kept: precomputed they held 20
+            // scalar registers through the loop
+            uint32_t kk0 = k0, kk1 = k1;
+            asm volatile("" : "+s"(kk0), "+s"(kk1));
+            const U4 x = philox4x32_10(U4{(uint32_t)g, st, u_id, 0u}, kk0, kk1);
             const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -130,12 +185,7 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
                 // even the largest noise this word allows cannot reach the bound: skip the logs
                 const float hi = sc + noise_bound(xs[j]);
                 if (hi + screen_margin(hi) < floor_t) {
-                    if (sc > mx) {
-                        z = z * __expf(mx - sc) + 1.0f;
-                        mx = sc;
-                    } else {
-                        z += __expf(sc - mx);
-                    }
+                    lse_push(mx, z, sc);
                     continue;
                 }
                 const float sa = sc + cheap_gumbel(xs[j]);
@@ -150,15 +200,37 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
                 } else {
                     floor_t = fmaxf(floor_t, sa - mg);
                 }
-                if (sc > mx) {
-                    z = z * __expf(mx - sc) + 1.0f;
-                    mx = sc;
-                } else {
-                    z += __expf(sc - mx);
-                }
+                lse_push(mx, z, sc);
             }
         }
         floor_w = wave_max_f(floor_t);
+    };
+    // Two groups in flight per lane, in two register sets that take turns: a set is
+    // copied out right after the other set's load has been issued (so the wait before the
+    // copy leaves that newer load in flight) and then refilled two groups ahead (copying a
+    // set that is still loading would make the compiler wait for it).
+    if (lane0 < n4) {  // one block for the set-up loads and the first copy (their order matters)
+        float set_a[4], set_b[4], l[4];
+        // (the scheduling barriers keep set_a's load first and its copy after set_b's load)
+        fetch_raw4<VEC4>(rs, threadIdx.x, set_a);
+        __builtin_amdgcn_sched_barrier(0);
+        fetch_raw4<VEC4>(rs, threadIdx.x + kThreads, set_b);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) l[j] = copy_out(set_a[j]);
+        fetch_raw4<VEC4>(rs, threadIdx.x + 2 * kThreads, set_a);
+        for (int g0 = lane0; g0 < n4; g0 += 2 * kThreads) {
+            const int g = g0 + (threadIdx.x & 63);
+            score4(l, g);
+            if (g0 + kThreads >= n4) break;  // wave-uniform
+#pragma unroll
+            for (int j = 0; j < 4; ++j) l[j] = copy_out(set_b[j]);
+            fetch_raw4<VEC4>(rs, g + 3 * kThreads, set_b);
+            score4(l, g + kThreads);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) l[j] = copy_out(set_a[j]);
+            fetch_raw4<VEC4>(rs, g + 4 * kThreads, set_a);
+        }
     }
     // wave merge
 #pragma unroll
@@ -196,7 +268,8 @@ sample_k(const float* __restrict__ logits, int64_t ld, int vocab, const int32_t*
     float lp = NAN, lse = NAN;
     if (best_i != 0x7FFFFFFF) {
         tok = best_i;
-        const float sc = UNIT_T ? row[tok] : div_rn(row[tok], temperature);
+        const float lt = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)tok * 4u, 0, 0));
+        const float sc = UNIT_T ? lt : div_rn(lt, temperature);
         const float lz = logf(z);
         lp = sc - mx - lz;
         lse = mx + lz;
@@ -251,12 +324,7 @@ logprob_gather_k(const float* __restrict__ logits, int64_t ld, int vocab, const 
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (!isfinite(l[j])) continue;
-            if (l[j] > mx) {
-                z = z * __expf(mx - l[j]) + 1.0f;
-                mx = l[j];
-            } else {
-                z += __expf(l[j] - mx);
-            }
+            lse_push(mx, z, l[j]);
         }
     }
 #pragma unroll
@@ -423,18 +491,27 @@ hipError_t launch_sample(const float* logits, int64_t ld, int rows, int vocab, c
                          float* traj_lp, int traj_ld, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     if (traj ? (lp_out || row_ml) : traj_lp != nullptr) return hipErrorInvalidValue;  // one output set per launch
-    const int vec4 = ((ld & 3) == 0 && ((uintptr_t)logits & 15) == 0) ? 1 : 0;
+    if (vocab <= 0 || vocab > (1 << 28)) return hipErrorInvalidValue;  // byte offsets of a row stay below 2^30
+    const bool vec4 = (ld & 3) == 0 && (vocab & 3) == 0 && ((uintptr_t)logits & 15) == 0;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-#define DASH_SAMPLE_LAUNCH(U, TR)                                                                                  \
-    sample_k<U, TR><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, k0, k1, tok_out, \
-                                               lp_out, row_ml, status, traj, traj_lp, traj_ld, vec4)
+#define DASH_SAMPLE_LAUNCH(U, TR, V4)                                                                          \
+    sample_k<U, TR, V4><<<rows, kThreads, 0, st>>>(logits, ld, vocab, row_of, uid, step, temperature, k0, k1,     \
+                                                   tok_out, lp_out, row_ml, status, traj, traj_lp, traj_ld)
+#define DASH_SAMPLE_LAUNCH_V(U, TR)     \
+    do {                                \
+        if (vec4)                       \
+            DASH_SAMPLE_LAUNCH(U, TR, true); \
+        else                            \
+            DASH_SAMPLE_LAUNCH(U, TR, false); \
+    } while (0)
     if (temperature == 1.0f) {
-        if (traj) DASH_SAMPLE_LAUNCH(true, true);
-        else DASH_SAMPLE_LAUNCH(true, false);
+        if (traj) DASH_SAMPLE_LAUNCH_V(true, true);
+        else DASH_SAMPLE_LAUNCH_V(true, false);
     } else {
-        if (traj) DASH_SAMPLE_LAUNCH(false, true);
-        else DASH_SAMPLE_LAUNCH(false, false);
+        if (traj) DASH_SAMPLE_LAUNCH_V(false, true);
+        else DASH_SAMPLE_LAUNCH_V(false, false);
     }
+#undef DASH_SAMPLE_LAUNCH_V
 #undef DASH_SAMPLE_LAUNCH
     return hipGetLastError();
 }

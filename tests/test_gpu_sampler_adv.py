@@ -93,6 +93,26 @@ def test_sample_row_of_stride_and_nonfinite():
     assert int(toks2.item()) == -1
 
 
+@pytest.mark.parametrize("V,ld,off", [(1000, 1003, 0), (4096, 4096, 1), (1001, 1004, 0), (151936, 151937, 0)])
+def test_sample_row_layouts(V, ld, off):
+    """Rows the sampler cannot read in 16-byte groups (a row stride or start that is not a
+    multiple of four floats, a vocabulary that is not) draw the same tokens as the oracle,
+    and as the same logits in an aligned copy (the two load paths agree)."""
+    R = 9
+    buf = synth.make_logits(R * ld + off + 4, 1, seed=V + ld).reshape(-1)
+    view = buf[off:off + R * ld].reshape(R, ld)[:, :V]
+    uid = np.arange(R, dtype=np.int32) * 13
+    step = np.full(R, 5, np.int32)
+    d = torch.from_numpy(buf).cuda()[off:off + R * ld].view(R, ld)[:, :V]
+    toks, lps = engine.sample(d, dev_i32(uid), dev_i32(step), 1.0, 77)
+    want_t, want_lp = osm.sample(np.ascontiguousarray(view), uid, step, 1.0, 77)
+    np.testing.assert_array_equal(toks.cpu().numpy(), want_t)
+    np.testing.assert_allclose(lps.cpu().numpy(), want_lp, atol=LP_ATOL, rtol=LP_RTOL)
+    t2, lp2 = engine.sample(torch.from_numpy(np.ascontiguousarray(view)).cuda(), dev_i32(uid), dev_i32(step), 1.0, 77)
+    np.testing.assert_array_equal(t2.cpu().numpy(), toks.cpu().numpy())
+    np.testing.assert_array_equal(lp2.cpu().numpy().view(np.uint32), lps.cpu().numpy().view(np.uint32))
+
+
 def test_sample_deterministic_and_independent_of_batch_position():
     logits = synth.make_logits(8, 151936, seed=5)
     uid = np.arange(8, dtype=np.int32)

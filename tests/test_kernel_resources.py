@@ -48,7 +48,7 @@ needs_hipcc = pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not av
 def test_sampler_scalar_registers():
     res = _resources("sampler.hip", "off")
     ks = {k: v for k, v in res.items() if "sample_k" in k}
-    assert len(ks) == 4, list(res)
+    assert len(ks) == 8, list(res)
     for name, r in ks.items():
         assert r["TotalSGPRs"] <= 80, (name, r)
         assert r.get("ScratchSize [bytes/lane]", 0) == 0, (name, r)
