@@ -168,6 +168,66 @@ def test_fullsize_concurrent_half_batches_bitexact(rollout_1p5b):
         L.dash_kv_release(kv.handle, slots)
 
 
+def test_concurrent_decode_steps_three_shapes_bitexact():
+    """Decode steps of the 0.5B, 1.5B and 3B layer widths (two layers each, the real
+    vocabulary) running at the same time on three streams, each with its own model, cache
+    and workspace, give the logits each gives alone, bit for bit, round after round.  The
+    row counts (512, 512, 1024) put the output projections and the 1.5B down projection on
+    the direct-to-LDS GEMM (64x64, 128x128 and 128x64 tiles), and the 1.5B step takes the
+    prefix-shared attention, whose prompt pages are copied from memory straight into LDS."""
+    require_gpu()
+    runs = []
+    for base, N in (("0.5b-b512", 512), ("1.5b-b1024", 512), ("3b-b1024", 1024)):
+        wl = synth.WORKLOADS[base]
+        s = dataclasses.replace(wl.shape, name=wl.shape.name + "-2layers", n_layers=2)
+        P, G, ps = wl.prompt_len, wl.group, 32
+        n_prompts = N // G
+        model = engine.Model(s, synth.make_weights(s, 8))
+        prompts = synth.make_prompts(dataclasses.replace(wl, shape=s, n_prompts=n_prompts), 8)
+        kv = engine.KVCache(model, ps, N, P + 1, n_prompts * (P // ps) + N + 8)
+        slots = list(range(N))
+        engine.prefill(model, kv, torch.from_numpy(prompts).cuda(), G, slots, ws=model.workspace(8 * P, 0))
+        L.dash_kv_reserve(kv.handle, slots, P + 1, engine.stream_handle())
+        r = dict(model=model, kv=kv, toks=dev_i32(np.random.default_rng(N).integers(0, s.vocab, N)),
+                 slots=dev_i32(np.arange(N)), pos=dev_i32(np.full(N, P)), ws=model.workspace(N, kv.max_ctx),
+                 out=torch.empty(N, s.vocab, dtype=torch.float32, device="cuda"),
+                 grouped=base.startswith("1.5b"), off=dev_i32(np.arange(n_prompts + 1) * G), G=G, P=P)
+        runs.append(r)
+
+    def step(r):
+        if r["grouped"]:
+            engine.decode_step_grouped(r["model"], r["kv"], r["toks"], r["slots"], r["pos"], r["off"], r["G"], r["P"],
+                                       r["ws"], r["out"])
+        else:
+            engine.decode_step(r["model"], r["kv"], r["toks"], r["slots"], r["pos"], r["ws"], r["out"])
+
+    refs = []
+    for r in runs:  # alone, one after another
+        step(r)
+        refs.append(r["out"].cpu().numpy())
+    streams = [torch.cuda.Stream() for _ in runs]
+    cur = torch.cuda.current_stream()
+    try:
+        for rnd in range(3):
+            for r in runs:
+                r["out"].fill_(float("nan"))
+            for st in streams:
+                st.wait_stream(cur)
+            for st, r in zip(streams, runs):
+                with torch.cuda.stream(st):
+                    step(r)
+            for st in streams:
+                cur.wait_stream(st)
+            for i, (r, ref) in enumerate(zip(runs, refs)):
+                got = r["out"].cpu().numpy()
+                bad = np.nonzero((got != ref).any(axis=1))[0]
+                assert bad.size == 0, f"round {rnd}, shape {i}: {bad.size} rows differ, first {bad[:8].tolist()}"
+    finally:
+        torch.cuda.synchronize()
+        for r in runs:
+            assert L.dash_kv_device_status(r["kv"].handle, engine.stream_handle()) == 0
+
+
 @pytest.mark.parametrize("base,rows", [("1.5b-b1024", 1024), ("3b-b2048", 2048)])
 def test_real_width_shallow_logits_strict(base, rows):
     """The real layer widths and vocabulary (1.5B: d 1536, d_ff 8960; 3B: d 2048, d_ff 11008;
