@@ -75,10 +75,21 @@ DASH_DEV float screen_margin(float sa) { return kScreenTol + fabsf(sa) * (1.0f /
 // terms, so the product's rounding stays far inside the margin added by the caller).
 DASH_DEV float noise_bound(uint32_t x) { return (float)(min(__clz(~x), 24) + 1) * 0.6931472f; }
 
+// Maximum over the wave's 64 lanes, returned wave-uniform: data-parallel-primitive moves
+// within each row of 16 lanes (quad swaps, then the half-row and row mirrors), row
+// broadcasts up to lane 63, then that lane read into a scalar register.  Every step is a
+// register move inside the vector unit; exchanges through LDS (one per xor distance)
+// each waited for the LDS round trip.
 DASH_DEV float wave_max_f(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    int x = __float_as_int(v);
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false))));
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false))));
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false))));
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false))));
+    // row_bcast15 into rows 1 and 3, row_bcast31 into rows 2 and 3 (rows not in the mask keep x)
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false))));
+    x = __float_as_int(fmaxf(__int_as_float(x), __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false))));
+    return __int_as_float(__builtin_amdgcn_readlane(x, 63));
 }
 
 // Raw words of entries 4g .. 4g+3 of a row through a buffer resource over the row:
