@@ -30,7 +30,7 @@ namespace {
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
 
-DASH_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
+DASH_DEV float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // ---- direct-to-LDS operand path ----------------------------------------------
 // Operand tiles can also go from memory straight into LDS (buffer_load ... lds, 16 bytes
