@@ -24,10 +24,11 @@
  *     last failure on the calling thread.
  *   - Pointers named d_* are device memory owned by the caller; h_* are host
  *     memory owned by the caller.  The library never allocates device memory:
- *     weights, KV pool, page table and workspaces are caller buffers (the only
- *     device memory of its own is a 4-byte variable of the diagnostic
- *     dash_sampler_check, part of the loaded code).  Handles (dash_model,
- *     dash_kv) are library-owned host objects; a dash_kv also owns a small
+ *     weights, KV pool, page table and workspaces are caller buffers.  Its only
+ *     device memory of its own is part of the loaded code: the 64 MiB workspace
+ *     array of dash_decode_step_noalloc and the small result variables of the
+ *     diagnostics dash_sampler_check and dash_bf16_round_check.  Handles
+ *     (dash_model, dash_kv) are library-owned host objects; a dash_kv also owns a small
  *     pinned host staging ring for page-table uploads, and kernel timing
  *     (dash_profile_enable) creates HIP events.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
@@ -327,6 +328,19 @@ int dash_sample(const float* d_logits, int64_t ld, int32_t n_rows, int32_t vocab
  * allocates nothing.
  */
 int dash_sampler_check(double* h_max_err, double* h_tol);
+
+/*
+ * Self-check of the bfloat16 rounding.  Every bf16 value the kernels store (weights
+ * aside: those come in bf16) is the round-to-nearest-even of a float32, which the
+ * kernels take from the GPU's conversion instruction; the bf16 storage points of
+ * the decoder (Sec. 4.1 runs it in bf16) are defined by that rounding.  This call
+ * converts all 2^32 float32 bit patterns on the current device and counts those
+ * whose result differs from integer rounding of the pattern (add 0x7FFF plus the
+ * lowest kept bit, truncate; NaNs keep their top half with the quiet bit set);
+ * 0 means the two agree everywhere.  Synchronous (null stream); the count is
+ * reduced into a device variable of the library, so the call allocates nothing.
+ */
+int dash_bf16_round_check(uint64_t* h_mismatches);
 
 /*
  * GRPO group advantage (Sec. 3.3, Eq. (4)) and gradient filter (Sec. 3.5).

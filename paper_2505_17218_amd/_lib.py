@@ -66,6 +66,7 @@ _SIGS = {
     "dash_sample": (C.c_int, [_P, C.c_int64, C.c_int32, C.c_int32, _P, _P, _P, C.c_float, C.c_uint64, _P, _P, _P,
                               _P, _P]),
     "dash_sampler_check": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+    "dash_bf16_round_check": (C.c_int, [C.POINTER(C.c_uint64)]),
     "dash_group_advantage_filter": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float, _P, _P,
                                               _P, _P]),
     "dash_live_compact": (C.c_int, [_P, _P, _P, _P, _P, _P, C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P, _P]),
@@ -254,6 +255,13 @@ def dash_rollout(model, kv, d_prompts, n_prompts, prompt_len, group, gen_len, bu
     b = i32_array(budgets) if budgets is not None else None
     _call("dash_rollout", model, kv, d_prompts, n_prompts, prompt_len, group, gen_len, b, C.c_float(temperature),
           C.c_uint64(seed), d_out_tokens, d_out_logprobs, int(use_graph), d_ws, ws_bytes, stream)
+
+
+def dash_bf16_round_check() -> int:
+    """Number of float32 inputs on which the kernels' bf16 conversion differs from integer rounding."""
+    n = C.c_uint64()
+    _call("dash_bf16_round_check", C.byref(n))
+    return n.value
 
 
 def dash_sampler_check() -> tuple[float, float]:

@@ -20,8 +20,15 @@ constexpr int kBufferDword3 = 0x00020000;
 
 DASH_DEV float bf2f(bf16_t u) { return __uint_as_float(static_cast<uint32_t>(u) << 16); }
 
-// float -> bfloat16, round to nearest even (NaN stays NaN).
-DASH_DEV bf16_t f2bf(float f) {
+// float -> bfloat16, round to nearest even (NaN stays NaN, with its quiet bit set): the
+// conversion instruction of gfx950 (v_cvt_pk_bf16_f32, two values per instruction).  It
+// gives the bits of integer rounding of the pattern (bf16_rne_bits) for every one of the
+// 2^32 inputs, NaNs included; dash_bf16_round_check verifies that on the device in use.
+DASH_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f)); }
+
+// The same rounding on the integer bit pattern: add 0x7FFF plus the lowest kept bit and
+// truncate; a NaN keeps its top half with the quiet bit set.
+DASH_DEV bf16_t bf16_rne_bits(float f) {
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
     u += 0x7FFFu + ((u >> 16) & 1u);

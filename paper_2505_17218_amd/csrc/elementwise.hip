@@ -264,6 +264,36 @@ hipError_t launch_embed_rmsnorm(int dtype, const int32_t* tok, const void* E, co
     return hipGetLastError();
 }
 
+// Inputs u * 256 + j (j < 256) per thread over all 2^32 float32 patterns: the count of
+// those whose f2bf result differs from bf16_rne_bits, reduced into a device variable of
+// this file (no allocation).
+namespace {
+
+__device__ unsigned long long g_bf16_mismatch;
+
+__global__ void bf16_round_check_k(unsigned long long* cnt) {
+    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;  // < 2^24
+    unsigned n = 0;
+    for (uint32_t j = 0; j < 256; ++j) {
+        const float f = __uint_as_float(t * 256u + j);
+        n += f2bf(f) != bf16_rne_bits(f);
+    }
+    if (n) atomicAdd(cnt, (unsigned long long)n);
+}
+
+}  // namespace
+
+hipError_t bf16_round_check(unsigned long long* mismatches) {
+    unsigned long long* d = nullptr;
+    hipError_t e = hipGetSymbolAddress((void**)&d, HIP_SYMBOL(g_bf16_mismatch));
+    if (e != hipSuccess) return e;
+    const unsigned long long zero = 0;
+    if ((e = hipMemcpy(d, &zero, 8, hipMemcpyHostToDevice)) != hipSuccess) return e;
+    bf16_round_check_k<<<(1u << 24) / 256, 256, 0, nullptr>>>(d);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return hipMemcpy(mismatches, d, 8, hipMemcpyDeviceToHost);
+}
+
 hipError_t launch_add_rmsnorm(int dtype, float* x, const float* delta, int nsplit, size_t split_stride,
                               const void* w, void* y, const int32_t* row_map, int rows, int d, float eps,
                               int write_x, hipStream_t st) {

@@ -121,6 +121,10 @@ hipError_t launch_prefill_attention(int dtype, const void* q, const int32_t* pos
                                     const int32_t* page_table, const void* pool, const KVGeom& g, int layer,
                                     int n_heads, void* o, int rows, int prompt_len, hipStream_t st);
 
+// Exhaustive check of f2bf against integer rounding of the bit pattern (synchronous, on
+// the null stream): the number of float32 inputs on which they differ.
+hipError_t bf16_round_check(unsigned long long* mismatches);
+
 // ---- sampling / advantage (sampler.hip, advantage.hip) ----
 // Screening tolerance of the sampler, and an exhaustive check of it (synchronous, on
 // the null stream): the largest |cheap noise - exact noise| over all noise values.

@@ -933,6 +933,15 @@ int dash_sampler_check(double* h_max_err, double* h_tol) {
     return DASH_OK;
 }
 
+int dash_bf16_round_check(uint64_t* h_mismatches) {
+    if (!h_mismatches) return fail(DASH_EINVAL, "dash_bf16_round_check: NULL argument");
+    unsigned long long n = 0;
+    const hipError_t e = bf16_round_check(&n);
+    if (e != hipSuccess) return fail(DASH_EDEVICE, "bf16 rounding check: %s", hipGetErrorString(e));
+    *h_mismatches = n;
+    return DASH_OK;
+}
+
 int dash_group_advantage_filter(const float* r, int32_t n_groups, int32_t group, int32_t mode, float eps, float tau,
                                 float* adv, int32_t* kept, int32_t* count, void* stream) {
     if (!r || !adv || !kept || !count) return fail(DASH_EINVAL, "dash_group_advantage_filter: NULL argument");

@@ -46,6 +46,13 @@ def test_sampler_screening_bound_exhaustive():
     assert 0.0 < err and 4.0 * err <= tol, (err, tol)
 
 
+def test_bf16_rounding_instruction_exhaustive():
+    """The GPU's float32 -> bfloat16 conversion, which every bf16 store of the kernels
+    uses, agrees with integer round-to-nearest-even of the bit pattern on all 2^32
+    inputs (NaNs included), on this device."""
+    assert L.dash_bf16_round_check() == 0
+
+
 @pytest.mark.parametrize("case", ["flat", "large", "near_ties", "cold", "two_level"])
 def test_sample_screening_adversarial(case):
     """Rows built so that many entries land close to the best score: flat logits (the
