@@ -94,6 +94,19 @@ DASH_DEV void attn_init(AttnState<HD>& st) {
     st.l = 0.f;
 }
 
+// Maximum over the four lanes of a column (lanes col, col+16, col+32, col+48), in every
+// one of them: the gfx950 lane-swap moves exchange 16-lane rows within each half, then the
+// halves, so both steps stay in the vector unit (an LDS permute each would put two LDS
+// round trips on every block's chain).  A swap of a value with itself hands each lane its
+// partner's value in one of the two results, and max is symmetric: the same bits as
+// max(x, x of lane ^ 16) then ^ 32.
+DASH_DEV float wave_max_cols(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // One block: keys key0 .. key0+31; this lane's column sees keys < lim; keys >= vlim
 // (wave-uniform) may hold stale data and have their V zeroed.
 template <int HD>
@@ -119,8 +132,7 @@ DASH_DEV void attn_block(AttnState<HD>& st, KVRegs<HD>& r, const bf16x8_t (&qf)[
             t[h * 4 + i] = v;
             mx = fmaxf(mx, v);
         }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = wave_max_cols(mx);
     const float m_new = fmaxf(st.m, mx);
     // a column with no visible key yet keeps m = -inf: use 0 as the reference so no NaN appears
     const float ref = m_new == -INFINITY ? 0.f : m_new;
