@@ -136,7 +136,10 @@ DASH_DEV void attn_block(AttnState<HD>& st, KVRegs<HD>& r, const bf16x8_t (&qf)[
     const float m_new = fmaxf(st.m, mx);
     // a column with no visible key yet keeps m = -inf: use 0 as the reference so no NaN appears
     const float ref = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(st.m - ref);
+    // the hardware exp2 (v_exp_f32): the library exp2f adds a rescaling step for results
+    // below 2^-126, which it would otherwise flush to zero; a probability that small
+    // changes none of the fp32 sums it enters (the largest entry contributes 1)
+    const float alpha = __builtin_amdgcn_exp2f(st.m - ref);
     st.m = m_new;
     // The probabilities enter the P.V MFMA as two bf16 operands, p = hi + lo with
     // hi = bf16(p) and lo = bf16(p - hi) (the difference is exact in fp32): the product
@@ -147,7 +150,7 @@ DASH_DEV void attn_block(AttnState<HD>& st, KVRegs<HD>& r, const bf16x8_t (&qf)[
     uint32_t pk[4], pl[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const float p0 = exp2f(t[2 * i] - ref), p1 = exp2f(t[2 * i + 1] - ref);
+        const float p0 = __builtin_amdgcn_exp2f(t[2 * i] - ref), p1 = __builtin_amdgcn_exp2f(t[2 * i + 1] - ref);
         psum += p0 + p1;
         const bf16_t h0 = f2bf(p0), h1 = f2bf(p1);
         pk[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
