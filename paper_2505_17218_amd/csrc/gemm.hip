@@ -207,7 +207,7 @@ DASH_DEV void qkv_epilogue(const f32x16_t* acc, float* Cs, const QkvRopeArgs& qa
     __syncthreads();
     const KVGeom& g = qa.g;
     const int hd = g.head_dim, half = hd >> 1;
-    const int lg_half = hd == 128 ? 6 : 5;
+    const int lg_half = hd == 128 ? 6 : 5, lg_hd = lg_half + 1;  // head indices by shifts, not divisions
     const int n0 = nt * BN;
     const int q_cols = qa.n_heads * hd, k_end = q_cols + g.n_kv * hd;
     if (n0 < k_end) {
@@ -223,11 +223,11 @@ DASH_DEV void qkv_epilogue(const f32x16_t* acc, float* Cs, const QkvRopeArgs& qa
             float lo, hi;
             rope_pair(a, b, pre.rope_cs[u].x, pre.rope_cs[u].y, lo, hi);
             if (n < q_cols) {
-                bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + n / hd) * hd;
+                bf16_t* q = qa.q_out + ((size_t)m * qa.n_heads + (n >> lg_hd)) * hd;
                 q[i] = f2bf(lo);
                 q[i + half] = f2bf(hi);
             } else if (row_page[rl] >= 0) {
-                bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) / hd, 0);
+                bf16_t* kb = qa.pool + kv_block(g, qa.layer, row_page[rl], (n - q_cols) >> lg_hd, 0);
                 // cache appends are non-temporal stores (see the v append below)
                 __builtin_nontemporal_store(f2bf(lo), &kb[k_index_bf16(g, row_key[rl], i)]);
                 __builtin_nontemporal_store(f2bf(hi), &kb[k_index_bf16(g, row_key[rl], i + half)]);
@@ -241,7 +241,7 @@ DASH_DEV void qkv_epilogue(const f32x16_t* acc, float* Cs, const QkvRopeArgs& qa
             const int rl = r0 + u * (NT / BN), m = m0 + rl;
             if (m >= M || n >= N || row_page[rl] < 0) continue;
             const float v = Cs[rl * CS + c] + pre.bias_a;
-            bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj / hd, 1);
+            bf16_t* vb = qa.pool + kv_block(g, qa.layer, row_page[rl], jj >> lg_hd, 1);
             // A decode step writes one key per row: 2 bytes into each of the 16-byte groups
             // of 8 keys, lines that later steps read from memory anyway.  Non-temporal
             // stores keep these partial lines out of L2: measured 8% less QKV time and 2%
