@@ -132,6 +132,44 @@ DASH_DEV void swiglu_epilogue(const f32x16_t* acc, bf16_t* H, int M, int N, int 
         }
 }
 
+// The same h through LDS: each wave writes its values of the BM x BN/2 output tile into
+// LDS (rows padded by 8 elements), then every thread stores whole 16-byte runs of 8
+// columns, so a tile row leaves as full lines instead of 2-byte stores per element.
+// Needs ldc and the tile's columns in whole runs of 8 and H 16-byte aligned (the caller
+// checks); Hs is dead operand LDS of at least BM * (BN/2 + 8) elements, and every wave
+// must be past its last read of it.
+template <int BM, int BN, int WGM, int WGN>
+DASH_DEV void swiglu_epilogue_lds(const f32x16_t* acc, bf16_t* Hs, bf16_t* H, int M, int N, int ldc, int m0, int nt,
+                                  int tid, int wr, int wc) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    constexpr int OW = BN / 2, OS = OW + 8;  // output tile width and LDS row stride (elements)
+    constexpr int RUNS = BM * OW / 8;        // 16-byte runs in the tile
+    static_assert(RUNS % NT == 0, "runs per thread");
+    const int lane = tid & 63;
+    const int rbase = (lane >> 5) * 4, ccol = lane & 31;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN / 2; ++j) {
+            const int c = wc * (WN / 2) + j * 32 + ccol;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rr = wr * WM + i * 32 + (r >> 2) * 8 + rbase + (r & 3);
+                Hs[rr * OS + c] = f2bf(silu(acc[i * TN + j][r]) * acc[i * TN + j + TN / 2][r]);
+            }
+        }
+    __syncthreads();
+    const int ff = N >> 1;
+#pragma unroll
+    for (int u = 0; u < RUNS / NT; ++u) {
+        const int run = tid + u * NT, rr = run / (OW / 8), c8 = (run % (OW / 8)) * 8;
+        const int m = m0 + rr, col = nt * OW + c8;
+        if (m < M && col < ff)
+            *reinterpret_cast<uint4*>(H + (size_t)m * ldc + col) = *reinterpret_cast<const uint4*>(Hs + rr * OS + c8);
+    }
+}
+
 // QKV epilogue inputs (fetched before the main loop so that their latency, for the k / v
 // tiles a dependent chain of position and slot, then the page table, hides behind it):
 // per tile row its cache page (or -1) and key within the page (row_page / row_key, LDS);
@@ -401,7 +439,13 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
                                              m0, nt, lane, wr, wc);
     } else {
         static_assert(EPI == EPI_SWIGLU, "unknown epilogue");
-        swiglu_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<bf16_t*>(C), M, N, ldc, m0, nt, lane, wr, wc);
+        static_assert(BM * (BN / 2 + 8) <= (int)(sizeof(As) / sizeof(bf16_t)), "h tile must fit the A operand LDS");
+        // whole 16-byte runs: ldc, the output width and the base all multiples of 8 elements
+        if (((ldc | (N >> 1)) & 7) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0)
+            swiglu_epilogue_lds<BM, BN, WGM, WGN>(&acc[0][0], &As[0][0], reinterpret_cast<bf16_t*>(C), M, N, ldc, m0, nt,
+                                                  tid, wr, wc);
+        else
+            swiglu_epilogue<BM, BN, WGM, WGN>(&acc[0][0], reinterpret_cast<bf16_t*>(C), M, N, ldc, m0, nt, lane, wr, wc);
     }
 }
 
