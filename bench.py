@@ -25,13 +25,13 @@ BF16_PEAK_TFLOPS = 2500.0
 
 # Memory traffic of one decode-attention launch of the 1.5B batch-1024 rollout, from the
 # rocprofv3 read/write request counters (profiles/decode_attn_traffic__1.5b-b1024.md:
-# 617.3 MB read + 3.15 MB written), valid for the attention sources it was measured with.
+# 616.1 MB read + 3.15 MB written), valid for the attention sources it was measured with.
 ATTN_TRAFFIC = {
     "workload": "1.5b-b1024",
-    "bytes_per_launch": 621_200_000,
+    "bytes_per_launch": 619_300_000,
     "sources": {
-        "paper_2505_17218_amd/csrc/attention.hip": "8797ed6308e9473008fe38b1ea497e707d0e0c0aa07e14fd7a6a31dd5a3e5a25",
-        "paper_2505_17218_amd/csrc/common.h": "16d56f2b1c378ddeb1902011b1b9beb198deb192709a5250858858f49c6d4547",
+        "paper_2505_17218_amd/csrc/attention.hip": "9491071fa82c907d9318b5fe6ffae46bb135cfe58f462320f4cd18102cd8a040",
+        "paper_2505_17218_amd/csrc/common.h": "0f40c78e53eca25bf8577dd7eee24736429eac2b540ae38e76c22c6b64ed8147",
     },
 }
 
