@@ -9,7 +9,10 @@
 // 20 ms, and each reports its median round: timing one variant after another instead
 // made whichever ran first up to 10% slower (clock ramp after the host-side set-up).
 //
-//   dash_gemm_bench [reps per round]
+//   dash_gemm_bench [reps per round] [small]
+//
+// With "small", the decode batches of one 64-row block (16, 32 and 64 rows) instead:
+// the tiles that stream the weights, with two to eight k-steps in flight per thread.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -140,12 +143,81 @@ bool same_bytes(const Dev& x, const Dev& y) {
     return a == b;
 }
 
+// Batches of one 64-row block: the projections stream their weights (every weight byte
+// read by one work-group) and each work-group's k-loop is a chain of dependent loads,
+// so the variants differ in how many k-steps each thread keeps in flight.
+void bench_small(const ModelShape* shapes, int n_shapes, int reps, hipStream_t st, std::mt19937& rng) {
+    constexpr int W = kWeightStream;
+    char label[128];
+    for (int si = 0; si < n_shapes; ++si) {
+        const ModelShape& sh = shapes[si];
+        const int d = sh.d, hq = sh.n_heads * sh.hd, qr = (sh.n_heads + 2 * sh.n_kv) * sh.hd;
+        for (int M : {16, 32, 64}) {
+            // QKV (unfused at this batch), output and down projections: fp32 stores
+            struct Proj {
+                const char* name;
+                int N, K;
+            };
+            const Proj projs[] = {{"qkv ", qr, d}, {"o   ", d, hq}, {"down", d, sh.ff}};
+            for (const Proj& pj : projs) {
+                const int N = pj.N, K = pj.K;
+                const int ns = gemm_pick_splits(1, EPI_STORE_F32, N, K);
+                Weights w(N, K, rng);
+                const size_t cn = (size_t)ns * M * N, ss = (size_t)M * N;
+                Dev a((size_t)M * K * 2), c0(cn * 4), c1(cn * 4);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"pd2", [&](const void* wp, bool r) { return run_bf16<64, 32, 2, 1, 2, EPI_STORE_F32, W>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"pd6", [&](const void* wp, bool r) { return run_bf16<64, 32, 2, 1, 6, EPI_STORE_F32, W>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"pd8", [&](const void* wp, bool r) { return run_bf16<64, 32, 2, 1, 8, EPI_STORE_F32, W>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"pd4cached", [&](const void* wp, bool r) { return run_bf16<64, 32, 2, 1, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                };
+                snprintf(label, sizeof label, "%-5s %s M=%4d N=%5d K=%5d s%d  ", sh.name, pj.name, M, N, K, ns);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            }
+            // gate/up projection with the SwiGLU epilogue
+            {
+                const int ff = sh.ff, N = 2 * ff, K = d;
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), c0((size_t)M * ff * 2), c1((size_t)M * ff * 2);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                const std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_SWIGLU, a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"64x128pd2", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 2, EPI_SWIGLU, W>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"64x128pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 4, EPI_SWIGLU, W>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"64x128pd6", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 6, EPI_SWIGLU, W>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"64x64pd2", [&](const void* wp, bool r) { return run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU, W>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"64x64pd4", [&](const void* wp, bool r) { return run_bf16<64, 64, 2, 1, 4, EPI_SWIGLU, W>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                };
+                snprintf(label, sizeof label, "%-5s gu   M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            }
+        }
+    }
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
     const int reps = argc > 1 ? atoi(argv[1]) : 20;
     const ModelShape shapes[] = {{"0.5b", 896, 14, 2, 64, 4864}, {"1.5b", 1536, 12, 2, 128, 8960},
                                  {"3b", 2048, 16, 2, 128, 11008}};
+    if (argc > 2 && strcmp(argv[2], "small") == 0) {
+        hipStream_t st;
+        CK(hipStreamCreate(&st));
+        std::mt19937 rng(7);
+        printf("kernel timings in us at 16-64 rows (weights cold, median of interleaved rounds); alternatives "
+               "marked = give the production bits\n");
+        bench_small(shapes, 3, reps, st, rng);
+        return 0;
+    }
     const int batches[] = {256, 512, 768, 1024, 2048};
     hipStream_t st;
     CK(hipStreamCreate(&st));
