@@ -262,6 +262,7 @@ int main(int argc, char** argv) {
                     {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
                     {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
                     {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"256x256w8", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
                 };
                 snprintf(label, sizeof label, "%-5s gu   M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
                 bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
@@ -282,6 +283,8 @@ int main(int argc, char** argv) {
                     {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
                     {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
                     {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"256x256w8", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
+                    {"256x256w8t", [&](const void* wp, bool r) { return run_bf16<256, 256, 2, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
                     {"lds128x128", [&](const void* wp, bool r) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, ns, ss, st); }},
                 };
                 snprintf(label, sizeof label, "%-5s down M=%4d N=%5d K=%5d s%d  ", sh.name, M, N, K, ns);
@@ -299,6 +302,8 @@ int main(int argc, char** argv) {
                 const std::vector<Variant> vs = {
                     {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
                     {"256x256w16", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"256x256w8", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                    {"256x256w8t", [&](const void* wp, bool r) { return run_bf16<256, 256, 2, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
                     {"128x256w16", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
                     {"256x128w8", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
                     {"lds128x128", [&](const void* wp, bool r) { return run_lds<128, 128, 2, 2, 4, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
