@@ -60,24 +60,34 @@ struct KVRegs {
 // Load the block of 32 keys starting at key `kin` of a page (kin % 32 == 0).
 // Buffer loads over the page's K and V blocks: an unbacked page gets an empty
 // range and reads as zeros, so the loads carry no branch and the next block can
-// be in flight while the current one is multiplied.
+// be in flight while the current one is multiplied.  Keys from `nvalid` on (past
+// the row's context in its last block) are not read: their K loads, and the V
+// loads of a lane group whose eight keys all lie there, take an offset past the
+// range and return zeros without touching memory.  Their scores are masked and
+// their V zeroed by the block step anyway, so the results are the same.
 template <int HD, int POLICY>
-DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps, int kin, bool ok, int col, int grp) {
+DASH_DEV void load_kv(KVRegs<HD>& r, const bf16_t* kb, const bf16_t* vb, int ps, int kin, bool ok, int col, int grp,
+                      int nvalid = 32) {
     const int bytes = ok ? ps * HD * 2 : 0;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(kb), 0, bytes, kBufferDword3);
     const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(vb), 0, bytes, kBufferDword3);
+    constexpr uint32_t kOut = 0x80000000u;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h) {
+        const bool kin_ctx = h * 16 + col < nvalid;
 #pragma unroll
-        for (int c = 0; c < HD / 32; ++c)
+        for (int c = 0; c < HD / 32; ++c) {
+            const uint32_t off = (uint32_t)(((c * ps + kin + h * 16 + col) * 32 + grp * 8) * 2);
             r.k[h][c] = __builtin_bit_cast(
-                uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (((c * ps + kin + h * 16 + col) * 32 + grp * 8) * 2), 0,
-                                                             POLICY));
+                uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, kin_ctx ? off : kOut, 0, POLICY));
+        }
+    }
+    const bool vin_ctx = grp * 4 < nvalid;  // keys grp*4 .. +3 and 16 + grp*4 .. +3
 #pragma unroll
-    for (int d = 0; d < HD / 16; ++d)
-        r.v[d] = __builtin_bit_cast(
-            uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, ((((kin >> 5) * 4 + grp) * HD + d * 16 + col) * 8) * 2, 0,
-                                                         POLICY));
+    for (int d = 0; d < HD / 16; ++d) {
+        const uint32_t off = (uint32_t)(((((kin >> 5) * 4 + grp) * HD + d * 16 + col) * 8) * 2);
+        r.v[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vin_ctx ? off : kOut, 0, POLICY));
+    }
 }
 
 template <int HD>
@@ -292,9 +302,9 @@ decode_attn_bf16_k(const bf16_t* __restrict__ q, const int32_t* __restrict__ pos
         const bf16_t* kb = pool + kv_block(g, layer, page, kvh, 0);
         const bf16_t* vb = pool + kv_block(g, layer, page, kvh, 1);
         if (key0 < g.shared_keys)  // wave-uniform: a prompt page the other rows of the group read too
-            load_kv<HD, kKvReuse>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
+            load_kv<HD, kKvReuse>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp, ctx - key0);
         else
-            load_kv<HD, kKvStream>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp);
+            load_kv<HD, kKvStream>(dst, kb, vb, g.page_size, key0 % g.page_size, ok, head, grp, ctx - key0);
     };
     if (!PRE || b_begin < b_end) {  // only a continued chain can be empty
         fetch(r[0], b_begin);
