@@ -25,12 +25,12 @@ BF16_PEAK_TFLOPS = 2500.0
 
 # Memory traffic of one decode-attention launch of the 1.5B batch-1024 rollout, from the
 # rocprofv3 read/write request counters (profiles/decode_attn_traffic__1.5b-b1024.md:
-# 616.1 MB read + 3.15 MB written), valid for the attention sources it was measured with.
+# 595.9 MB read + 3.15 MB written), valid for the attention sources it was measured with.
 ATTN_TRAFFIC = {
     "workload": "1.5b-b1024",
-    "bytes_per_launch": 619_300_000,
+    "bytes_per_launch": 599_100_000,
     "sources": {
-        "paper_2505_17218_amd/csrc/attention.hip": "9491071fa82c907d9318b5fe6ffae46bb135cfe58f462320f4cd18102cd8a040",
+        "paper_2505_17218_amd/csrc/attention.hip": "d7872754a3c4d32096cb2a52c0acccfe6ab0adc3234586060611604122336633",
         "paper_2505_17218_amd/csrc/common.h": "0f40c78e53eca25bf8577dd7eee24736429eac2b540ae38e76c22c6b64ed8147",
     },
 }
