@@ -578,3 +578,53 @@ def test_grouped_decode_matches_oracle(shape, n_prompts, G, P, T):
     run = run_stepwise(model, kv, prompts, G, T, 1.0, 19, grouped=True)
     worst = _check_run(shape, w, prompts, G, T, run, 1.0, 19, TOL[shape.dtype])
     print(f"grouped {shape.name} P={P}: max |dlogits| = {worst:.3g}")
+
+
+@pytest.mark.parametrize("shape,P,T", [(BF16_B, 45, 24), (BF16_A, 33, 40)])
+def test_stale_nonfinite_pool_bytes_do_not_change_results(shape, P, T):
+    """Cache bytes past a row's context (the unused slots of its last page, pages never
+    written) are never used: with every pool byte set to a bf16 NaN pattern before the
+    prefill, the stepwise decode (per-row and prefix-shared attention), the graph-replayed
+    rollout and the teacher-forced recompute give the same bits as with a zeroed pool.
+    Contexts run through partial last pages (P, P + T not multiples of the page size),
+    where the decode kernel skips the loads past the context and zeroes V there."""
+    n_prompts, G = 2, 4
+    N = n_prompts * G
+    w = synth.make_weights(shape, 5)
+    wl = synth.Workload("t", shape, n_prompts, G, P, T)
+    prompts = synth.make_prompts(wl, 5)
+    model = engine.Model(shape, w)
+
+    def fresh_kv(nan: bool):
+        kv = make_kv(model, 32, N, P + T)
+        if nan:
+            kv.pool.view(torch.int16).fill_(0x7FC0)
+            torch.cuda.synchronize()
+        return kv
+
+    runs = {}
+    for nan in (False, True):
+        for grouped in (False, True):
+            kv = fresh_kv(nan)
+            runs[nan, grouped] = run_stepwise(model, kv, prompts, G, T, 1.0, 11, grouped=grouped)
+            kv.close()
+    for grouped in (False, True):
+        a, b = runs[False, grouped], runs[True, grouped]
+        np.testing.assert_array_equal(a.tokens, b.tokens)
+        assert np.array_equal(a.logits.view(np.uint32), b.logits.view(np.uint32)), f"grouped={grouped}"
+        assert np.array_equal(a.logprobs.view(np.uint32), b.logprobs.view(np.uint32))
+
+    outs = {}
+    for nan in (False, True):
+        kv = fresh_kv(nan)
+        ro = engine.Rollout(model, kv, n_prompts, P, G, T)
+        toks, lps = ro.run(dev_i32(prompts), 1.0, 11, use_graph=True)
+        seqs = torch.cat([dev_i32(np.repeat(prompts, G, axis=0)), toks], dim=1)
+        kv.close()
+        kv = fresh_kv(nan)
+        tf = engine.teacher_forced_logprobs(model, kv, seqs, P)
+        kv.close()
+        outs[nan] = (toks.cpu().numpy(), lps.cpu().numpy(), tf.cpu().numpy())
+    for x, y in zip(outs[False], outs[True]):
+        assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+    np.testing.assert_array_equal(outs[True][0], runs[True, False].tokens)
