@@ -26,6 +26,7 @@
 #include <string>
 #include <vector>
 
+#include "elementwise.hip"
 #include "gemm.hip"
 
 #define CK(x)                                                                                          \
@@ -143,6 +144,63 @@ bool same_bytes(const Dev& x, const Dev& y) {
     return a == b;
 }
 
+// The QKV projection with the fused bias / RoPE / KV-append epilogue on M rows: one
+// page per row in a one-layer pool (two copies, reference and scratch), positions 5..31.
+struct QkvCase {
+    const ModelShape& sh;
+    int M, N, K, hd;
+    Weights w;
+    Dev a, bias, cs, pos, slot, table, status, pool0, pool1, q0, q1;
+    KVGeom g;
+    QkvCase(const ModelShape& s, int m, std::mt19937& rng)
+        : sh(s), M(m), N((s.n_heads + 2 * s.n_kv) * s.hd), K(s.d), hd(s.hd), w(N, K, rng), a((size_t)M * K * 2),
+          bias((size_t)N * 2), cs((size_t)M * hd * 4), pos((size_t)M * 4), slot((size_t)M * 4), table((size_t)M * 4),
+          status(256), pool0(pool_bytes()), pool1(pool_bytes()), q0((size_t)M * s.n_heads * hd * 2),
+          q1((size_t)M * s.n_heads * hd * 2), g{1, M, s.n_kv, hd, 32, 1, M, 2048, 0} {
+        const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+        const auto hb = randn_bf16(N, 0.02f, rng);
+        CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+        CK(hipMemcpy(bias.p, hb.data(), hb.size() * 2, hipMemcpyHostToDevice));
+        std::vector<int32_t> hp(M), hs(M), ht(M);
+        std::vector<float> hcs((size_t)M * hd);
+        for (int r = 0; r < M; ++r) {
+            hp[r] = 5 + r % 27;
+            hs[r] = r;
+            ht[r] = r;
+            for (int i = 0; i < hd / 2; ++i) {
+                const double ang = hp[r] * std::pow(1e6, -2.0 * i / hd);
+                hcs[((size_t)r * (hd / 2) + i) * 2] = (float)std::cos(ang);
+                hcs[((size_t)r * (hd / 2) + i) * 2 + 1] = (float)std::sin(ang);
+            }
+        }
+        CK(hipMemcpy(pos.p, hp.data(), M * 4, hipMemcpyHostToDevice));
+        CK(hipMemcpy(slot.p, hs.data(), M * 4, hipMemcpyHostToDevice));
+        CK(hipMemcpy(table.p, ht.data(), M * 4, hipMemcpyHostToDevice));
+        CK(hipMemcpy(cs.p, hcs.data(), hcs.size() * 4, hipMemcpyHostToDevice));
+        CK(hipMemset(status.p, 0, 4));
+        CK(hipMemset(pool0.p, 0, pool0.n));
+        CK(hipMemset(pool1.p, 0, pool1.n));
+    }
+    size_t pool_bytes() const { return (size_t)M * sh.n_kv * 2 * 32 * sh.hd * 2; }  // one page per row, one layer
+    QkvRopeArgs args(bool ref) const {
+        return QkvRopeArgs{(const bf16_t*)bias.p, (const float*)cs.p, (const int32_t*)pos.p, (const int32_t*)slot.p,
+                           (const int32_t*)table.p, (bf16_t*)(ref ? pool0.p : pool1.p), g, 0,
+                           (bf16_t*)(ref ? q0.p : q1.p), sh.n_heads, (uint32_t*)status.p};
+    }
+    // times the variants (0 = reference) and checks q and the appended K/V against it
+    void run(const char* label, const std::vector<Variant>& vs, int reps, hipStream_t st) {
+        bench_case(label, vs, w, reps, st,
+                   [&] {
+                       CK(hipMemset(pool1.p, 0, pool1.n));
+                       CK(hipMemset(q1.p, 0xFF, q1.n));
+                   },
+                   [&] { return same_bytes(q0, q1) && same_bytes(pool0, pool1); });
+        uint32_t hst = 0;
+        CK(hipMemcpy(&hst, status.p, 4, hipMemcpyDeviceToHost));
+        if (hst) printf("  (status set!)\n");
+    }
+};
+
 // Batches of one 64-row block: the projections stream their weights (every weight byte
 // read by one work-group) and each work-group's k-loop is a chain of dependent loads,
 // so the variants differ in how many k-steps each thread keeps in flight.
@@ -198,6 +256,30 @@ void bench_small(const ModelShape* shapes, int n_shapes, int reps, hipStream_t s
                 snprintf(label, sizeof label, "%-5s gu   M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
                 bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
                            [&] { return same_bytes(c0, c1); });
+            }
+            // the QKV projection with its fused epilogue (at these batches the decode step runs
+            // the unfused projection and a separate RoPE / append kernel instead)
+            if (gemm_qkv_fusable(1, sh.n_heads, sh.n_kv, sh.hd)) {
+                QkvCase c(sh, M, rng);
+                const void* A = c.a.p;
+                const int N = c.N, K = c.K;
+                Dev qkv32((size_t)M * N * 4);
+                const std::vector<Variant> vs = {
+                    // the decode step's path at these batches: projection to fp32, then the RoPE / append kernel
+                    {"unfused", [&](const void* wp, bool r) -> hipError_t {
+                         const QkvRopeArgs qa = c.args(r);
+                         const hipError_t e = launch_gemm(1, EPI_STORE_F32, A, wp, qkv32.p, M, N, K, N, 1, 0, st);
+                         if (e != hipSuccess) return e;
+                         return launch_qkv_rope_append(1, (const float*)qkv32.p, 1, 0, qa.bias, qa.cs, qa.pos, qa.slot,
+                                                       qa.page_table, qa.pool, qa.g, 0, qa.q_out, M, qa.n_heads, qa.status, st);
+                     }},
+                    {"fused64x128", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, c.args(r)); }},
+                    {"stream", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE, W>(A, wp, nullptr, M, N, K, 0, 1, 0, st, c.args(r)); }},
+                    {"stream_pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 4, EPI_QKV_ROPE, W>(A, wp, nullptr, M, N, K, 0, 1, 0, st, c.args(r)); }},
+                    {"stream_w4pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 4, EPI_QKV_ROPE, W>(A, wp, nullptr, M, N, K, 0, 1, 0, st, c.args(r)); }},
+                };
+                snprintf(label, sizeof label, "%-5s qkvf M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
+                c.run(label, vs, reps, st);
             }
         }
     }
@@ -314,64 +396,24 @@ int main(int argc, char** argv) {
             }
             // ---- QKV projection with bias, RoPE and the KV append (fused epilogue)
             if (gemm_qkv_fusable(1, sh.n_heads, sh.n_kv, sh.hd)) {
-                const int N = qr, K = d, hd = sh.hd, ps = 32;
-                Weights w(N, K, rng);
-                Dev a((size_t)M * K * 2), bias((size_t)N * 2), cs((size_t)M * hd * 4);
-                Dev pos((size_t)M * 4), slot((size_t)M * 4), table((size_t)M * 4), status(256);
-                const size_t pool_elems = (size_t)M * sh.n_kv * 2 * ps * hd;  // one page per row, one layer
-                Dev pool0(pool_elems * 2), pool1(pool_elems * 2), q0((size_t)M * hq * 2), q1((size_t)M * hq * 2);
-                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
-                const auto hb = randn_bf16(N, 0.02f, rng);
-                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
-                CK(hipMemcpy(bias.p, hb.data(), hb.size() * 2, hipMemcpyHostToDevice));
-                std::vector<int32_t> hp(M), hs(M), ht(M);
-                std::vector<float> hcs((size_t)M * hd);
-                for (int m = 0; m < M; ++m) {
-                    hp[m] = 5 + m % 27;
-                    hs[m] = m;
-                    ht[m] = m;
-                    for (int i = 0; i < hd / 2; ++i) {
-                        const double ang = hp[m] * std::pow(1e6, -2.0 * i / hd);
-                        hcs[((size_t)m * (hd / 2) + i) * 2] = (float)std::cos(ang);
-                        hcs[((size_t)m * (hd / 2) + i) * 2 + 1] = (float)std::sin(ang);
-                    }
-                }
-                CK(hipMemcpy(pos.p, hp.data(), M * 4, hipMemcpyHostToDevice));
-                CK(hipMemcpy(slot.p, hs.data(), M * 4, hipMemcpyHostToDevice));
-                CK(hipMemcpy(table.p, ht.data(), M * 4, hipMemcpyHostToDevice));
-                CK(hipMemcpy(cs.p, hcs.data(), hcs.size() * 4, hipMemcpyHostToDevice));
-                CK(hipMemset(status.p, 0, 4));
-                CK(hipMemset(pool0.p, 0, pool0.n));
-                CK(hipMemset(pool1.p, 0, pool1.n));
-                const KVGeom g{1, M, sh.n_kv, hd, ps, 1, M, 2048, 0};
-                auto args = [&](bool ref) {
-                    return QkvRopeArgs{(const bf16_t*)bias.p, (const float*)cs.p, (const int32_t*)pos.p,
-                                       (const int32_t*)slot.p, (const int32_t*)table.p,
-                                       (bf16_t*)(ref ? pool0.p : pool1.p), g, 0, (bf16_t*)(ref ? q0.p : q1.p),
-                                       sh.n_heads, (uint32_t*)status.p};
-                };
+                QkvCase c(sh, M, rng);
+                const int N = qr, K = d;
+                auto args = [&](bool ref) { return c.args(ref); };
+                const void* A = c.a.p;
                 const std::vector<Variant> vs = {
                     // the production path: fused above its size threshold, else the unfused GEMM + RoPE kernel
                     {"production", [&](const void* wp, bool r) -> hipError_t {
-                         if (gemm_qkv_fuse_pays(M, N)) return launch_gemm_qkv_rope(a.p, wp, M, N, K, args(r), st);
-                         return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r));
+                         if (gemm_qkv_fuse_pays(M, N)) return launch_gemm_qkv_rope(A, wp, M, N, K, args(r), st);
+                         return run_bf16<64, 128, 2, 4, 2, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r));
                      }},
-                    {"lds64x128", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
-                    {"lds64x128s3", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
-                    {"64x128pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
-                    {"64x128pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 4, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
-                    {"64x128w4pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 3, EPI_QKV_ROPE>(a.p, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"lds64x128", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 4, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"lds64x128s3", [&](const void* wp, bool r) { return run_lds<64, 128, 2, 2, 3, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 3, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128pd4", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 4, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
+                    {"64x128w4pd3", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 3, EPI_QKV_ROPE>(A, wp, nullptr, M, N, K, 0, 1, 0, st, args(r)); }},
                 };
                 snprintf(label, sizeof label, "%-5s qkv  M=%4d N=%5d K=%5d     ", sh.name, M, N, K);
-                bench_case(label, vs, w, reps, st,
-                           [&] {
-                               CK(hipMemset(pool1.p, 0, pool1.n));
-                               CK(hipMemset(q1.p, 0xFF, q1.n));
-                           },
-                           [&] { return same_bytes(q0, q1) && same_bytes(pool0, pool1); });
-                uint32_t hst = 0;
-                CK(hipMemcpy(&hst, status.p, 4, hipMemcpyDeviceToHost));
-                if (hst) printf("  (status set!)\n");
+                c.run(label, vs, reps, st);
             }
         }
     }
