@@ -12,7 +12,9 @@
 //   dash_gemm_bench [reps per round] [small]
 //
 // With "small", the decode batches of one 64-row block (16, 32 and 64 rows) instead:
-// the tiles that stream the weights, with two to eight k-steps in flight per thread.
+// the tiles that stream the weights, with two to eight k-steps in flight per thread,
+// and the fused QKV kernel against the projection followed by the RoPE / KV-append
+// kernel of elementwise.hip (the path the decode step takes at these batches).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
