@@ -299,7 +299,7 @@ DASH_DEV void qkv_epilogue(const f32x16_t* acc, float* Cs, const QkvRopeArgs& qa
 template <int BM, int BN, int WGM, int WGN, int PD, int EPI, int WPOL = 0>
 __global__ void __launch_bounds__(64 * WGM * WGN)
 gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __restrict__ C, int M, int N, int K,
-             int ldc, int m_tiles, int n_tiles, int kps, size_t split_stride, QkvRopeArgs qa) {
+             int ldc, int m_tiles, int n_tiles, int nt0, int kps, size_t split_stride, QkvRopeArgs qa) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
     constexpr int A_CH = BM * 8 / NT, B_CH = BN * 8 / NT;  // 16-byte chunks per thread per k-step
@@ -313,7 +313,7 @@ gemm_bf16_k(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, void* __
     const int w = xcd_remap(blockIdx.x, gridDim.x);
     const int mt = w % m_tiles;
     const int rest = w / m_tiles;
-    const int nt = rest % n_tiles;
+    const int nt = nt0 + rest % n_tiles;  // a launch may cover the column tiles from nt0 on
     const int split = rest / n_tiles;
     const int m0 = mt * BM;
     const int k_begin = split * kps;
@@ -629,7 +629,23 @@ hipError_t run_bf16(const void* A, const void* W, void* C, int M, int N, int K, 
     if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
     const int blocks = m_tiles * n_tiles * nsplit;
     gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI, WPOL><<<blocks, 64 * WGM * WGN, 0, st>>>(
-        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, kps, split_stride, qa);
+        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, 0, kps, split_stride, qa);
+    return hipGetLastError();
+}
+
+// Gate/up with the SwiGLU epilogue over output columns [col0, col1) of h only (col0 a
+// multiple of the tile's BN / 2 output columns): the same tiles, hence the same bits, as
+// the launch over every column.
+template <int BM, int BN, int WGM, int WGN, int PD>
+hipError_t run_bf16_swiglu_cols(const void* A, const void* W, void* C, int M, int N, int K, int ldc, int col0,
+                                int col1, hipStream_t st) {
+    constexpr int tn = BN / 2;
+    if (col0 % tn || col0 < 0 || col1 <= col0 || col1 > N / 2) return hipErrorInvalidValue;
+    if (K % kBK || (size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
+    const int m_tiles = (M + BM - 1) / BM;
+    const int n_tiles = (col1 - col0 + tn - 1) / tn;
+    gemm_bf16_k<BM, BN, WGM, WGN, PD, EPI_SWIGLU><<<m_tiles * n_tiles, 64 * WGM * WGN, 0, st>>>(
+        (const bf16_t*)A, (const bf16_t*)W, C, M, N, K, ldc, m_tiles, n_tiles, col0 / tn, K, 0, QkvRopeArgs{});
     return hipGetLastError();
 }
 
@@ -745,6 +761,29 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
         if (epi == EPI_SWIGLU) {
             if (nsplit != 1) return hipErrorInvalidValue;
             if (M > 384) {
+                const int ff = N / 2;
+                const long mb = (M + 255) / 256;
+                const long t256_all = mb * ((ff + 127) / 128);
+                const long split_tiles = t256_all / 256 * 256 / mb;  // column tiles of the whole rounds
+                if (t256_all > 256 && t256_all < 4 * 256 && t256_all % 256 && t256_all % 256 < 128 &&
+                    split_tiles >= 1) {
+                    // Whole rounds of 256x256 tiles leave a last round under half full: those
+                    // rounds run as one launch over the columns they cover, the remaining
+                    // columns as a second launch on the largest of 128x256, 128x128 and 64x128
+                    // tiles that still gives it 128 or more work-groups (else 64x128).  Measured
+                    // with dash_gemm_bench at 1024 and 2048 rows: 1.5B 70.9 -> 63.6 us and
+                    // 132.1 -> 117.6 us, 3B at 1024 rows 108.7 -> 98.9 us, 0.5B at 2048 rows
+                    // 44.9 -> 42.7 us (a last round at least half full runs whole, as below).
+                    const int c_split = (int)split_tiles * 128;
+                    hipError_t e = run_bf16_swiglu_cols<256, 256, 4, 4, 2>(A, W, C, M, N, K, ldc, 0, c_split, st);
+                    if (e != hipSuccess) return e;
+                    const long rc = ff - c_split, m128 = (M + 127) / 128;
+                    if (m128 * ((rc + 127) / 128) >= 128)
+                        return run_bf16_swiglu_cols<128, 256, 4, 4, 2>(A, W, C, M, N, K, ldc, c_split, ff, st);
+                    if (m128 * ((rc + 63) / 64) >= 128)
+                        return run_bf16_swiglu_cols<128, 128, 4, 2, 2>(A, W, C, M, N, K, ldc, c_split, ff, st);
+                    return run_bf16_swiglu_cols<64, 128, 2, 2, 2>(A, W, C, M, N, K, ldc, c_split, ff, st);
+                }
                 // Past 384 rows the tile is chosen by how its work-groups fill the 256 CUs
                 // (one 256x256 or 128x256 work-group per CU, two 128x128 ones): 256x256 where
                 // they fill one round (128-256 tiles), or leave a last round at least half

@@ -287,6 +287,48 @@ void bench_small(const ModelShape* shapes, int n_shapes, int reps, hipStream_t s
     }
 }
 
+// Gate/up at 512-2048 rows, cut by columns: the 256x256 tiles of the whole rounds (256 of
+// them per round) timed on their own, and the remaining columns on smaller tiles, each on a
+// projection of that width.  The sum estimates a two-launch split against the production
+// tiling of the whole width.
+void bench_gu_split(const ModelShape* shapes, int n_shapes, int reps, hipStream_t st, std::mt19937& rng) {
+    char label[160];
+    for (int si = 0; si < n_shapes; ++si) {
+        const ModelShape& sh = shapes[si];
+        for (int M : {1024, 2048}) {
+            const int K = sh.d, mb = (M + 255) / 256;
+            const int round_cols = 256 / mb * 128;  // h columns of one round of 256x256 tiles
+            const int full = sh.ff / round_cols * round_cols, rest = sh.ff - full;
+            auto one = [&](int ff, const char* what, bool split_variants) {
+                const int N = 2 * ff;
+                Weights w(N, K, rng);
+                Dev a((size_t)M * K * 2), c0((size_t)M * ff * 2), c1((size_t)M * ff * 2);
+                const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+                CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+                auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+                std::vector<Variant> vs = {
+                    {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_SWIGLU, a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                    {"256x256", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }},
+                };
+                if (split_variants) {
+                    vs.push_back({"128x128", [&](const void* wp, bool r) { return run_bf16<128, 128, 4, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }});
+                    vs.push_back({"64x128", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 2, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }});
+                    vs.push_back({"64x64", [&](const void* wp, bool r) { return run_bf16<64, 64, 2, 1, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }});
+                    vs.push_back({"128x256", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_SWIGLU>(a.p, wp, out(r), M, N, K, ff, 1, 0, st); }});
+                }
+                snprintf(label, sizeof label, "%-5s gu %-9s M=%4d ff=%5d     ", sh.name, what, M, ff);
+                bench_case(label, vs, w, reps, st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                           [&] { return same_bytes(c0, c1); });
+            };
+            one(sh.ff, "whole", false);
+            if (full > 0 && rest > 0) {
+                one(full, "rounds", false);
+                one(rest, "rest", true);
+            }
+        }
+    }
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -300,6 +342,14 @@ int main(int argc, char** argv) {
         printf("kernel timings in us at 16-64 rows (weights cold, median of interleaved rounds); alternatives "
                "marked = give the production bits\n");
         bench_small(shapes, 3, reps, st, rng);
+        return 0;
+    }
+    if (argc > 2 && strcmp(argv[2], "split") == 0) {
+        hipStream_t st;
+        CK(hipStreamCreate(&st));
+        std::mt19937 rng(7);
+        printf("gate/up kernel timings in us by column range (weights cold, median of interleaved rounds)\n");
+        bench_gu_split(shapes, 3, reps, st, rng);
         return 0;
     }
     const int batches[] = {256, 512, 768, 1024, 2048};

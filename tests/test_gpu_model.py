@@ -194,16 +194,16 @@ def test_bf16_swiglu_tile_regimes_bitexact():
         assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
 
 
-# d_ff = 8320 (65 columns of 128-wide SwiGLU tile pairs): at 1024 rows neither one round of
-# 256x256 tiles (260 > 256) nor 128x256 tiles with a well-filled last round (520 = 2 x 256 + 8)
-# fit, so gate/up runs on 128x128 tiles; 40 rows on 64x64 tiles
+# d_ff = 8320 (65 columns of 128-wide SwiGLU tile pairs): at 1024 rows one round of 256x256
+# tiles covers 8192 columns (260 tiles would leave a last round of 4), so gate/up runs as two
+# launches, 256x256 over those columns and 64x128 over the last 128; 40 rows on 64x64 tiles
 BF16_I = synth.Shape("bf16-ff8320", 1, 256, 4, 2, 64, 8320, 500, 1e6, synth.DT_BF16)
 
 
 def test_bf16_swiglu_tile_rounds_bitexact():
-    """The 1024-row gate/up tiling chosen by how the tiles fill the GPU (128x128 here) gives
-    the rows it shares with a 40-row batch the same logits, bit for bit, and matches the
-    oracle."""
+    """The 1024-row gate/up tiling chosen by how the tiles fill the GPU (one round of
+    256x256 tiles, the remaining columns on 64x128 tiles) gives the rows it shares with a
+    40-row batch the same logits, bit for bit, and matches the oracle."""
     shape = BF16_I
     w = synth.make_weights(shape, 12)
     wl = synth.Workload("t", shape, 256, 4, 10, 2)
@@ -248,6 +248,29 @@ def test_bf16_gemm_regimes_across_batch_sizes_bitexact():
         run = runs[n_prompts]
         ref = om.rollout_logits(sd, w, prompts[n // 4], run.tokens[n])
         assert np.abs(ref - run.logits[:, n, :]).max() <= TOL[shape.dtype], (n_prompts, n)
+
+
+@pytest.mark.parametrize("ff,n_prompts,rest", [(8960, 256, "64x128"), (8960, 512, "128x128"),
+                                              (11008, 256, "128x256"), (4864, 512, "128x128")])
+def test_bf16_swiglu_column_split_bitexact(ff, n_prompts, rest):
+    """Gate/up widths of the 0.5B, 1.5B and 3B shapes at 1024 and 2048 rows, where whole
+    rounds of 256x256 tiles would leave a last round under half full: the columns of the
+    whole rounds run as one launch and the rest (on the tile named by `rest`) as another.
+    The rows shared with a 40-row batch (64x64 tiles) get the same logits bit for bit, and
+    sampled rows match the oracle."""
+    shape = synth.Shape(f"bf16-ff{ff}", 1, 256, 4, 2, 64, ff, 500, 1e6, synth.DT_BF16)
+    w = synth.make_weights(shape, 13)
+    wl = synth.Workload("t", shape, n_prompts, 4, 10, 2)
+    prompts = synth.make_prompts(wl, 13)
+    model = engine.Model(shape, w)
+    N = 4 * n_prompts
+    big = run_stepwise(model, make_kv(model, 32, N, 12), prompts, 4, 2, 1.0, 5)
+    small = run_stepwise(model, make_kv(model, 32, 40, 12), prompts[:10], 4, 2, 1.0, 5)
+    np.testing.assert_array_equal(small.logits[1], big.logits[1][:40])  # the decode step (M = N vs 40)
+    sd = shape_dict(shape)
+    for n in (0, N // 2 + 1, N - 1):
+        ref = om.rollout_logits(sd, w, prompts[n // 4], big.tokens[n])
+        assert np.abs(ref - big.logits[:, n, :]).max() <= TOL[shape.dtype], n
 
 
 # vocab 9000 (>= 8192 columns: the LM head's tiles): 64x256 up to 64 rows, 128x256 up to 128,
