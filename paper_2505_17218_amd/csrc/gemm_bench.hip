@@ -327,6 +327,36 @@ void bench_gu_split(const ModelShape* shapes, int n_shapes, int reps, hipStream_
             }
         }
     }
+    // the 1.5B LM head (151,936 columns, fp32 logits) the same way
+    for (int M : {1024, 2048}) {
+        const int K = 1536, V = 151936, mb = (M + 255) / 256;
+        const int full = (int)((long)mb * ((V + 255) / 256) / 256 * 256 / mb) * 256, rest = V - full;
+        auto one = [&](int N, const char* what, bool split_variants) {
+            Weights w(N, K, rng);
+            Dev a((size_t)M * K * 2), c0((size_t)M * N * 4), c1((size_t)M * N * 4);
+            const auto ha = randn_bf16((size_t)M * K, 1.f, rng);
+            CK(hipMemcpy(a.p, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+            auto out = [&](bool ref) { return ref ? c0.p : c1.p; };
+            std::vector<Variant> vs = {
+                {"production", [&](const void* wp, bool r) { return launch_gemm(1, EPI_STORE_F32, a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+                {"256x256", [&](const void* wp, bool r) { return run_bf16<256, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }},
+            };
+            if (split_variants) {
+                vs.push_back({"128x256", [&](const void* wp, bool r) { return run_bf16<128, 256, 4, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }});
+                vs.push_back({"128x128", [&](const void* wp, bool r) { return run_bf16<128, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }});
+                vs.push_back({"256x128", [&](const void* wp, bool r) { return run_bf16<256, 128, 4, 2, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }});
+                vs.push_back({"64x128", [&](const void* wp, bool r) { return run_bf16<64, 128, 2, 4, 2, EPI_STORE_F32>(a.p, wp, out(r), M, N, K, N, 1, 0, st); }});
+            }
+            snprintf(label, sizeof label, "1.5b  lm %-9s M=%4d N=%6d     ", what, M, N);
+            bench_case(label, vs, w, std::max(2, reps / 8), st, [&] { CK(hipMemset(c1.p, 0xFF, c1.n)); },
+                       [&] { return same_bytes(c0, c1); });
+        };
+        one(V, "whole", false);
+        if (full > 0 && rest > 0) {
+            one(full, "rounds", false);
+            one(rest, "rest", true);
+        }
+    }
 }
 
 }  // namespace
