@@ -771,9 +771,9 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, const void* W, void* C
                     // rounds run as one launch over the columns they cover, the remaining
                     // columns as a second launch on the largest of 128x256, 128x128 and 64x128
                     // tiles that still gives it 128 or more work-groups (else 64x128).  Measured
-                    // with dash_gemm_bench at 1024 and 2048 rows: 1.5B 70.9 -> 63.6 us and
-                    // 132.1 -> 117.6 us, 3B at 1024 rows 108.7 -> 98.9 us, 0.5B at 2048 rows
-                    // 44.9 -> 42.7 us (a last round at least half full runs whole, as below).
+                    // with dash_gemm_bench at 1024 and 2048 rows: 1.5B 70.9 -> 63.0 us and
+                    // 132.1 -> 114.5 us, 3B at 1024 rows 108.7 -> 96.9 us, 0.5B at 2048 rows
+                    // 44.9 -> 43.0 us (a last round at least half full runs whole, as below).
                     const int c_split = (int)split_tiles * 128;
                     hipError_t e = run_bf16_swiglu_cols<256, 256, 4, 4, 2>(A, W, C, M, N, K, ldc, 0, c_split, st);
                     if (e != hipSuccess) return e;
