@@ -251,11 +251,13 @@ def test_bf16_gemm_regimes_across_batch_sizes_bitexact():
 
 
 @pytest.mark.parametrize("ff,n_prompts,rest", [(8960, 256, "64x128"), (8960, 512, "128x128"),
-                                              (11008, 256, "128x256"), (4864, 512, "128x128")])
+                                              (11008, 256, "128x256"), (4864, 512, "128x128"),
+                                              (8960, 275, "128x256")])
 def test_bf16_swiglu_column_split_bitexact(ff, n_prompts, rest):
     """Gate/up widths of the 0.5B, 1.5B and 3B shapes at 1024 and 2048 rows, where whole
     rounds of 256x256 tiles would leave a last round under half full: the columns of the
-    whole rounds run as one launch and the rest (on the tile named by `rest`) as another.
+    whole rounds run as one launch and the rest (on the tile named by `rest`) as another
+    (1100 rows, 275 prompts: partial row tiles in both launches, columns split at 6528).
     The rows shared with a 40-row batch (64x64 tiles) get the same logits bit for bit, and
     sampled rows match the oracle."""
     shape = synth.Shape(f"bf16-ff{ff}", 1, 256, 4, 2, 64, ff, 500, 1e6, synth.DT_BF16)
